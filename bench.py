@@ -1,0 +1,192 @@
+"""Benchmark of the STRIDE scoring / early-stop / restart path on one MI355X.
+
+One step = stride_score -> stride_stop -> stride_restart_turn over one batch of
+synthetic rollouts whose logits are already resident in HBM.  Prints one JSON
+line with scored tokens/s, the roofline of the dominant kernel (the row
+scoring kernel, timed with HIP events on the stream it runs on) and the
+float64 CPU oracle timed on a bounded sample of the same workload.
+
+    python bench.py [--steps K] [--warmup W] [--workload agentic|reasoning|multi|tiny]
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+METRIC = "scored tokens/sec (logp+KL+stop scan) and % of HBM peak, 1 MI355X"
+PARAMS = os.path.join(ROOT, "tests", "golden", "workload_params.json")
+TRAFFIC = os.path.join(ROOT, "profiles", "traffic.json")
+SCORE_SRC = os.path.join(ROOT, "paper_2609_14636_amd", "csrc", "score.hip")
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def workload_params(name: str, seed: int):
+    with open(PARAMS) as f:
+        p = json.load(f)
+    key = f"{name}:{seed}"
+    if key not in p["workloads"]:
+        raise SystemExit(f"no thresholds for {key} in {PARAMS}")
+    e = p["workloads"][key]
+    return [float(x) for x in e["lambda"]], [float(x) for x in e["alpha"]]
+
+
+def source_digest() -> str:
+    with open(SCORE_SRC, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def measured_traffic(workload: str, bytes_alg: float):
+    """HBM bytes per launch of the scoring kernel from committed rocprofv3 counters, if they were
+    taken on the current kernel source; else None."""
+    if not os.path.exists(TRAFFIC):
+        return None
+    with open(TRAFFIC) as f:
+        t = json.load(f)
+    e = t.get(workload)
+    if not e or e.get("score_hip_sha256_16") != source_digest():
+        return None
+    return float(e["bytes_per_launch"])
+
+
+def cpu_baseline(wl, lam, alpha, budget_rows: int):
+    """Float64 oracle on whole rollouts of the workload (at least one), compute time only."""
+    from tests import harness as H
+
+    threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+    rows, rs = 0, []
+    for r in range(wl.n_rollouts):
+        a, b = wl.rollout_rows(r)
+        if rs and rows + (b - a) > budget_rows:
+            break
+        rs.append(r)
+        rows += b - a
+    t_gen, t_ora = 0.0, 0.0
+    for r in rs:
+        a, b = wl.rollout_rows(r)
+        t0 = time.perf_counter()
+        t = wl.teacher_rows_host(a, b - a, threads)
+        s = wl.student_rows_host(a, b - a, threads)
+        t1 = time.perf_counter()
+        sc = H.OP.score(t, s, wl.tok[a:b], wl.vocab)
+        H.oracle_rollout(wl, r, sc, lam, alpha)
+        t2 = time.perf_counter()
+        del t, s
+        t_gen += t1 - t0
+        t_ora += t2 - t1
+    return {"value": rows / t_ora, "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "sample": f"rollouts {rs[0]}..{rs[-1]} of the timed workload ({rows} tokens, "
+                      f"{2 * rows} logit rows of V={wl.vocab}); oracle compute {t_ora:.1f} s, "
+                      f"input generation {t_gen:.1f} s not counted"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="agentic",
+                    choices=["tiny", "agentic", "reasoning", "multi"])
+    ap.add_argument("--seed", type=int, default=1001)
+    ap.add_argument("--cpu-rows", type=int, default=6000,
+                    help="bound on the oracle sample (token rows; whole rollouts, at least one)")
+    ap.add_argument("--no-cpu", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only: --gpus {args.gpus} is not supported "
+              "(the path shards by rollout with no exchange; see DESIGN.md)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import paper_2609_14636_amd as P
+    from synth import workloads as W
+    from tests import harness as H
+
+    torch.cuda.set_device(0)
+    wl = W.make(args.workload, seed=args.seed)
+    lam, alpha = workload_params(args.workload, args.seed)
+    log(f"[bench] workload {args.workload} seed {args.seed}: R={wl.n_rollouts} T={wl.n_turns} "
+        f"N={wl.n_tokens} V={wl.vocab}; generating {2 * wl.logits_bytes() / 1e9:.1f} GB on device")
+    inp = H.device_inputs(wl)
+    path = P.Path(inp["layout"], wl.unit, with_student=True)
+    stream = torch.cuda.current_stream()
+    torch.cuda.synchronize()
+
+    def step():
+        path.score(wl.vocab, inp["teachers"], inp["student"], inp["ids"])
+        path.stop(lam, inp["start"])
+        path.restart(alpha, inp["mask"])
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    log(f"[bench] warmup done ({args.warmup} steps)")
+
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        ev[i][0].record(stream)
+        path.score(wl.vocab, inp["teachers"], inp["student"], inp["ids"])
+        ev[i][1].record(stream)
+        path.stop(lam, inp["start"])
+        path.restart(alpha, inp["mask"])
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    ms_step = (t1 - t0) * 1e3 / args.steps
+    score_ms = sum(a.elapsed_time(b) for a, b in ev) / args.steps
+    out = path.host()
+    if out["flags"] != 0:
+        raise SystemExit(f"device flags {out['flags']:#x} on the benchmark workload")
+    H.assert_invariants(out, wl)
+    log(f"[bench] {args.steps} steps: {ms_step:.3f} ms/step, scoring {score_ms:.3f} ms; "
+        f"stops {int((out['stop_unit'] >= 0).sum())}/{wl.n_rollouts}")
+
+    n_tok = wl.n_tokens
+    per_token = 2 * wl.vocab * wl.esize + 4 + 8  # two logit rows in, token id in, two logps out
+    bytes_alg = per_token * n_tok
+    achieved = bytes_alg / (score_ms * 1e-3) / 1e9
+    traffic = measured_traffic(args.workload, bytes_alg)
+    res = {
+        "metric": METRIC,
+        "value": n_tok / (ms_step * 1e-3),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if wl.dtype == W.BF16 else "f32",
+        "data": "synthetic",
+        "config": {"workload": f"{args.workload}: {wl.n_rollouts} rollouts x {wl.n_turns} turns, "
+                               f"{n_tok} scored tokens, V={wl.vocab}, teacher+student logits",
+                   "global_batch": wl.n_rollouts, "seq_len": int(n_tok // max(wl.n_rollouts, 1)),
+                   "parallelism": "single GPU"},
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
+                     "kernel": "score_rows_kernel<bf16>", "kernel_ms": score_ms,
+                     "bytes_per_launch": bytes_alg},
+    }
+    if not args.no_cpu:
+        log("[bench] timing the float64 oracle on a bounded sample")
+        res["cpu_baseline"] = cpu_baseline(wl, lam, alpha, args.cpu_rows)
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

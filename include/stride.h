@@ -1,0 +1,186 @@
+/*
+ * stride.h -- C ABI of libstride.so: the data-parallel hot path of STRIDE's
+ * on-policy distillation step on one AMD Instinct MI355X (gfx950).
+ *
+ * Paper: "Know When to Stop, Where to Restart: Accelerating Multi-Turn Agentic
+ * On-Policy Distillation" (STRIDE).  The path scores student rollouts with the
+ * teacher and the student (Eq. 1, Sec. 3.1-3.2), averages the teacher
+ * log-probability per turn (Eq. 4), applies the early-stop test (Eq. 5,
+ * Sec. 4.1, with token units for the single-turn variant of Sec. 5.5) and
+ * picks the restart turn of the prefix buffer (Sec. 4.2, Eq. 6, Algorithm 1).
+ *
+ * Conventions shared by every entry point
+ *   - Pointers are device pointers unless marked (host).  The caller owns every
+ *     buffer; the library keeps no state between calls and allocates nothing.
+ *     Scratch memory is the caller's workspace `ws` of at least
+ *     stride_workspace_size() bytes, 256-byte aligned, used in stream order.
+ *   - Calls are asynchronous on `stream` and never synchronise.  Two calls that
+ *     share a workspace must be ordered (same stream, or events).
+ *   - Argument errors (null pointers, negative sizes, misaligned rows, too small
+ *     a workspace, unsupported dtype) are found on the host before anything is
+ *     launched: the call returns a non-OK status, launches nothing, and
+ *     stride_last_error() describes the problem.
+ *   - Data errors found on the device are OR-ed into *dev_flags (a device
+ *     uint32, may be NULL) and the call still completes; the affected outputs
+ *     are NaN (or -1 for indices).  Read dev_flags after synchronising.
+ *   - Layout: the scored tokens of all rollouts form one stream of N rows in
+ *     rollout order.  Rollout r owns turns [rollout_turn_off[r],
+ *     rollout_turn_off[r+1]); turn k owns rows [turn_tok_off[k],
+ *     turn_tok_off[k+1]).  Only tokens the student generated are rows: the
+ *     environment's observation tokens are masked out of the loss (Eq. 2) and
+ *     are not part of the stream.  Indices of turns and units returned per
+ *     rollout are 0-based and local to the rollout; the paper's 1-based k*
+ *     is k_star + 1, and its K0 = k* - 1 equals k0.
+ *   - Units: STRIDE_UNIT_TURN makes each turn a unit whose value is its mean
+ *     teacher log-probability (Eq. 4, Eq. 5); STRIDE_UNIT_TOKEN makes each row
+ *     a unit whose value is its teacher log-probability (Sec. 5.5).
+ */
+#ifndef STRIDE_H
+#define STRIDE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    STRIDE_OK = 0,
+    STRIDE_ERR_INVALID_ARG = 1, /* a null pointer, a negative size, inconsistent sizes   */
+    STRIDE_ERR_UNSUPPORTED = 2, /* dtype, alignment or a size past the library limits    */
+    STRIDE_ERR_WORKSPACE = 3,   /* ws is NULL, misaligned or smaller than required       */
+    STRIDE_ERR_HIP = 4          /* a HIP launch failed; the message names the HIP error  */
+} stride_status;
+
+enum { STRIDE_BF16 = 0, STRIDE_F32 = 1 };          /* logits element type         */
+enum { STRIDE_UNIT_TURN = 0, STRIDE_UNIT_TOKEN = 1 };
+
+/* Device data-error flags, OR-ed into *dev_flags. */
+enum {
+    STRIDE_FLAG_TOKEN_OOB = 1,   /* token id outside [0, vocab): that row's outputs are NaN        */
+    STRIDE_FLAG_EMPTY_TURN = 2,  /* a turn with no rows: its mean is NaN                            */
+    STRIDE_FLAG_BAD_OFFSETS = 4, /* offsets not monotone, not starting at 0 or not ending at N/T    */
+    STRIDE_FLAG_NONFINITE = 8,   /* a row holds NaN or +inf, or only -inf: its outputs are NaN      */
+    STRIDE_FLAG_BAD_DOMAIN = 16, /* domain[r] outside [0, n_teachers) or [0, n_dom)                 */
+    STRIDE_FLAG_SPIN_LIMIT = 32  /* a cross-workgroup wait gave up; the scan results are not valid  */
+};
+
+#define STRIDE_MAX_DOMAINS 64
+
+typedef struct {
+    int32_t n_rollouts;              /* R >= 0                                        */
+    int32_t n_turns;                 /* T >= 0                                        */
+    int64_t n_tokens;                /* N >= 0, rows of every logits matrix           */
+    const int32_t *rollout_turn_off; /* [R+1], 0 .. T, non-decreasing                 */
+    const int64_t *turn_tok_off;     /* [T+1], 0 .. N, non-decreasing                 */
+    const int32_t *domain;           /* [R] teacher / lambda / alpha index, NULL => 0 */
+} stride_layout;
+
+/*
+ * Bytes of workspace the calls below need for this layout and unit (the
+ * maximum over stride_score, stride_score_fused, stride_stop and
+ * stride_restart_turn, so one buffer serves them all).  Host-only; reads only
+ * the sizes in *layout.  Returns 0 for a NULL layout.
+ */
+size_t stride_workspace_size(const stride_layout *layout, int32_t unit);
+
+/*
+ * Teacher and student scoring of every row, then the per-turn mean.
+ * Eq. (1) (Sec. 3.1): log pi(y_t | y_<t) is the log-softmax of the row's
+ * logits at the sampled token y_t, for the teacher (T) and the student (S);
+ * Sec. 3.2: the per-token KL estimate is log pi_S(y_t) - log pi_T(y_t) = -r_t;
+ * Eq. (4): lbar_k = (1/n_k) sum over turn k's rows of log pi_T.
+ *
+ *   vocab            V >= 1 logits per row; rows have ld >= V elements, row-major
+ *   ld               row stride in elements; ld * element size must be a multiple
+ *                    of 16 bytes, and every logits pointer 16-byte aligned
+ *   dtype            STRIDE_BF16 or STRIDE_F32
+ *   n_teachers       1 .. STRIDE_MAX_DOMAINS
+ *   teacher_logits   (host) array of n_teachers device pointers, each [N, ld];
+ *                    the rows of rollout r are read from teacher domain[r]
+ *                    (rows of rollouts routed elsewhere are never read)
+ *   student_logits   [N, ld] or NULL (then logp_s and kl must be NULL)
+ *   token_ids        [N] int32, the sampled tokens
+ *   logp_t, logp_s   [N] float outputs (logp_s may be NULL)
+ *   kl               [N] float output log pi_S - log pi_T, or NULL
+ *   turn_mean        [T] double output
+ *   dev_flags        device uint32 or NULL
+ */
+stride_status stride_score(const stride_layout *layout, int32_t vocab, int64_t ld, int32_t dtype,
+                           int32_t n_teachers, const void *const *teacher_logits,
+                           const void *student_logits, const int32_t *token_ids, float *logp_t,
+                           float *logp_s, float *kl, double *turn_mean, uint32_t *dev_flags,
+                           void *ws, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * As stride_score, with the teacher's logits produced by its output
+ * projection inside the kernel and never written to memory: z = h W with h
+ * the teacher's final hidden state of the row and W its lm_head, followed by
+ * the same log-softmax at the sampled token (Eq. 1).  The student's logits
+ * are given as in stride_score.
+ *
+ *   d                hidden size, a multiple of 64
+ *   hidden_t         [N, d] bf16 row-major
+ *   w_t              [d, vocab] bf16 row-major (ld of W = vocab, a multiple of 8)
+ *   student_logits   [N, ld] bf16 or NULL
+ */
+stride_status stride_score_fused(const stride_layout *layout, int32_t vocab, int32_t d,
+                                 const void *hidden_t, const void *w_t, const void *student_logits,
+                                 int64_t ld, const int32_t *token_ids, float *logp_t, float *logp_s,
+                                 float *kl, double *turn_mean, uint32_t *dev_flags, void *ws,
+                                 size_t ws_bytes, hipStream_t stream);
+
+/*
+ * Early-stop test, Eq. (5) (Sec. 4.1), over the new units of each rollout:
+ * C_u = sum_{j=K0}^{u} value_j for u >= K0 = start_unit[r] (the prefix reused
+ * from an earlier rollout is left out of the sum, Sec. 4.1 and Algorithm 1);
+ * stop_unit[r] is the first u >= K0 with C_u < lambda[domain[r]], strictly,
+ * or -1.  The triggering unit is kept for the loss.
+ *
+ *   unit              STRIDE_UNIT_TURN (values = turn_mean, double [T]) or
+ *                     STRIDE_UNIT_TOKEN (values = logp_t, float [N])
+ *   lambda            (host) [n_dom] thresholds, n_dom in 1 .. STRIDE_MAX_DOMAINS
+ *   start_unit        [R] int32 K0 per rollout (clamped to [0, units]), or NULL => 0
+ *   cum               [U] double output: C_u, and 0 for u < K0
+ *   stop_unit         [R] int32 output
+ *   n_retained_tokens [R] int64 output or NULL: rows of units K0 .. stop
+ *                     (K0 .. last unit without a stop), the newly generated rows
+ *                     that join the loss
+ * Sums are carried in double; results do not depend on scheduling.
+ */
+stride_status stride_stop(const stride_layout *layout, int32_t unit, const void *values,
+                          const double *lambda, int32_t n_dom, const int32_t *start_unit,
+                          double *cum, int32_t *stop_unit, int64_t *n_retained_tokens,
+                          uint32_t *dev_flags, void *ws, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * Prefix-buffer restart pick (Sec. 4.2 steps 1-3, Eq. 6, Algorithm 1) from the
+ * record of each rollout: its units 0 .. stop_unit[r] (all units when
+ * stop_unit is NULL or stop_unit[r] = -1).  Unit u is correct iff
+ * correct_mask[u] != 0 (NULL => every unit) and value_u > alpha[domain[r]],
+ * strictly.  k_max[r] is the length of the leading run of correct units;
+ * k_star[r] is the lowest index u < k_max attaining the minimum value (-1 if
+ * k_max = 0); k0[r] = max(k_star, 0) is the number of units the next rollout
+ * reuses as context.
+ *
+ *   unit, values      as in stride_stop
+ *   alpha             (host) [n_dom]; -INFINITY disables the gate
+ *   correct_mask      [U] uint8 or NULL
+ *   k_star, k0        [R] int32 outputs;  k_max [R] int32 output or NULL
+ */
+stride_status stride_restart_turn(const stride_layout *layout, int32_t unit, const void *values,
+                                  const int32_t *stop_unit, const double *alpha, int32_t n_dom,
+                                  const uint8_t *correct_mask, int32_t *k_star, int32_t *k0,
+                                  int32_t *k_max, uint32_t *dev_flags, hipStream_t stream);
+
+/* Message for the last non-OK status returned on this thread ("" if none). */
+const char *stride_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* STRIDE_H */

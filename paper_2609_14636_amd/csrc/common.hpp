@@ -1,0 +1,75 @@
+// common.hpp -- declarations shared by the HIP sources of libstride.so.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+#include "../../include/stride.h"
+
+namespace stride {
+
+constexpr int kWave = 64;
+
+// Device-side view of the host's per-domain tables, passed by value.
+struct DomainTable {
+    double v[STRIDE_MAX_DOMAINS];
+};
+struct PtrTable {
+    const void *p[STRIDE_MAX_DOMAINS];
+};
+
+// Scan tile descriptor published by one tile and read by its successors.
+struct alignas(16) TileDesc {
+    double value;     // sum of the tile's values after its last segment head
+    uint32_t head;    // 1 if a segment starts inside the tile
+    uint32_t status;  // 0 = not yet published, 1 = aggregate ready
+};
+
+// Workspace layout (byte offsets from ws, each region 256-byte aligned).
+struct WsLayout {
+    size_t counter;   // uint32 tile counter + spare words
+    size_t row_dom;   // uint8 [N] teacher index per row (multi-teacher scoring)
+    size_t unit_off;  // int64 [R+1] first unit of each rollout
+    size_t desc;      // TileDesc [tiles]
+    size_t fused;     // float2 [N, vocab tiles] partial (max, sum) of the fused projection
+    size_t total;
+};
+
+constexpr int kScanThreads = 256;
+constexpr int kScanItems = 8;
+constexpr int64_t kScanTile = (int64_t)kScanThreads * kScanItems;
+
+WsLayout ws_layout(int64_t n_rollouts, int64_t n_tokens, int64_t n_units, int64_t fused_partials);
+
+__device__ inline void raise_flag(uint32_t *flags, uint32_t bits) {
+    if (flags) atomicOr(flags, bits);
+}
+
+// ---- launchers (one per source file); all asynchronous on `stream` ----
+
+// score.hip
+hipError_t launch_row_domain(const stride_layout &L, int32_t n_teachers, uint8_t *row_dom,
+                             uint32_t *flags, hipStream_t stream);
+hipError_t launch_score_rows(int32_t dtype, const PtrTable &teachers, int32_t n_teachers,
+                             const uint8_t *row_dom, const void *student, const int32_t *ids,
+                             float *logp_t, float *logp_s, int64_t n_rows, int32_t vocab,
+                             int64_t ld, uint32_t *flags, hipStream_t stream);
+
+// turn.hip
+hipError_t launch_turn_mean(const stride_layout &L, const float *logp_t, const float *logp_s,
+                            float *kl, double *turn_mean, uint32_t *flags, hipStream_t stream);
+
+// scan.hip
+hipError_t launch_stop(const stride_layout &L, int32_t unit, const void *values,
+                       const DomainTable &lambda, int32_t n_dom, const int32_t *start,
+                       double *cum, int32_t *stop_unit, int64_t *retained, uint32_t *flags,
+                       void *ws, hipStream_t stream);
+
+// restart.hip
+hipError_t launch_restart(const stride_layout &L, int32_t unit, const void *values,
+                          const int32_t *stop_unit, const DomainTable &alpha, int32_t n_dom,
+                          const uint8_t *mask, int32_t *k_star, int32_t *k0, int32_t *k_max,
+                          uint32_t *flags, hipStream_t stream);
+
+}  // namespace stride

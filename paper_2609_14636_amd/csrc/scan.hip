@@ -1,0 +1,323 @@
+// scan.hip -- the early-stop test: per-rollout cumulative sums and first crossing.
+//
+// Eq. (5) (Sec. 4.1): stop at the first unit K* whose cumulative value is
+// strictly below lambda; with a reused prefix of K0 units the sum starts at
+// unit K0 (Sec. 4.1, prefix-buffer synergy; Algorithm 1).  Units are turns
+// (values = lbar_k, Eq. 4) or tokens (values = teacher log-probabilities, the
+// single-turn variant of Sec. 5.5), so one rollout can hold tens of thousands
+// of units.
+//
+// Single-pass segmented scan (Merrill and Garland, "Single-pass Parallel Prefix
+// Scan with Decoupled Look-back", 2016), specialised for determinism:
+//   1. A workgroup takes the next tile id from a counter (tiles start in id
+//      order, so every tile waited on is already running: forward progress).
+//   2. It loads 2048 units, zeroes those before K0, and scans them in double
+//      (per-thread sequential, then a fixed shuffle tree, then waves in order),
+//      with the segmented operator (f1,v1)+(f2,v2) = (f1|f2, f2 ? v2 : v1+v2).
+//   3. It publishes its aggregate (value after its last rollout start, and
+//      whether one occurs) with a release store, before waiting on anything.
+//   4. If its first unit continues a rollout, it looks back over predecessor
+//      aggregates only, nearest first, until the tile holding that rollout's
+//      start.  Inclusive prefixes are never used, so every sum is associated
+//      in the same order on every run: cum is bit-reproducible.
+//   5. The first crossing per rollout is an integer min, reduced in LDS and
+//      then with one global atomicMin per rollout per tile.
+// Waits are bounded: past the spin limit the tile gives up, raises
+// STRIDE_FLAG_SPIN_LIMIT and writes NaN, so no wave can hang.
+#include <climits>
+
+#include "common.hpp"
+
+namespace stride {
+namespace {
+
+constexpr int kSlots = 256;            // rollouts per tile reduced in LDS
+constexpr uint32_t kSpinLimit = 1u << 22;
+
+struct StopArgs {
+    stride_layout L;
+    DomainTable lambda;
+    int32_t n_dom;
+    int32_t unit;
+    int64_t n_units;
+    int64_t n_tiles;
+    const void *values;
+    const int32_t *start;
+    const int64_t *unit_off;  // [R+1] in the workspace
+    double *cum;
+    int32_t *stop_unit;
+    int64_t *retained;
+    uint32_t *counter;
+    TileDesc *desc;
+    uint32_t *flags;
+};
+
+// unit_off, stop_unit sentinels, descriptor reset, tile counter reset.
+__global__ __launch_bounds__(256) void stop_prep_kernel(StopArgs a, int64_t *unit_off) {
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    const int64_t R = a.L.n_rollouts, T = a.L.n_turns;
+    if (i <= R) {
+        int64_t t = a.L.rollout_turn_off[i];
+        bool bad = t < 0 || t > T;
+        if (i == 0 && t != 0) bad = true;
+        if (i == R && t != T) bad = true;
+        if (i < R && a.L.rollout_turn_off[i + 1] < t) bad = true;
+        t = t < 0 ? 0 : (t > T ? T : t);
+        unit_off[i] = (a.unit == STRIDE_UNIT_TURN) ? t : a.L.turn_tok_off[t];
+        if (bad) raise_flag(a.flags, STRIDE_FLAG_BAD_OFFSETS);
+    }
+    if (i < R) a.stop_unit[i] = INT_MAX;
+    if (i < a.n_tiles) {
+        a.desc[i].status = 0;
+        a.desc[i].head = 0;
+        a.desc[i].value = 0.0;
+    }
+    if (i == 0) *a.counter = 0;
+}
+
+struct Seg {
+    uint32_t f;
+    double v;
+};
+
+__device__ __forceinline__ Seg combine(Seg a, Seg b) {
+    return Seg{a.f | b.f, b.f ? b.v : a.v + b.v};
+}
+
+__device__ __forceinline__ int64_t find_rollout(const int64_t *off, int64_t R, int64_t u) {
+    // last r in [0, R) with off[r] <= u; -1 if none
+    if (R == 0 || off[0] > u) return -1;
+    int64_t lo = 0, hi = R;
+    while (hi - lo > 1) {
+        const int64_t mid = (lo + hi) >> 1;
+        if (off[mid] <= u) lo = mid; else hi = mid;
+    }
+    return lo;
+}
+
+template <typename VT>
+__global__ __launch_bounds__(kScanThreads) void stop_scan_kernel(StopArgs a) {
+    __shared__ int64_t s_tile;
+    __shared__ Seg s_wave[kScanThreads / kWave];
+    __shared__ double s_carry;
+    __shared__ int32_t s_first[kSlots];
+    __shared__ int64_t s_r0;
+
+    const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
+    if (tid == 0) s_tile = (int64_t)atomicAdd(a.counter, 1u);
+    for (int i = tid; i < kSlots; i += blockDim.x) s_first[i] = INT_MAX;
+    __syncthreads();
+    const int64_t tile = s_tile;
+    const int64_t u0 = tile * kScanTile;
+    const int64_t R = a.L.n_rollouts;
+    const VT *vals = static_cast<const VT *>(a.values);
+
+    // ---- load and thread-local segmented scan ----
+    const int64_t ubase = u0 + (int64_t)tid * kScanItems;
+    int64_t r = find_rollout(a.unit_off, R, ubase);
+    if (tid == 0) s_r0 = find_rollout(a.unit_off, R, u0);
+    double run[kScanItems];
+    uint8_t head[kScanItems];
+    int64_t rr[kScanItems];
+    Seg tagg{0u, 0.0};
+#pragma unroll
+    for (int j = 0; j < kScanItems; ++j) {
+        const int64_t u = ubase + j;
+        double v = 0.0;
+        uint8_t h = 0;
+        int64_t rj = -1;  // rollout holding unit u, -1 if none (only with bad offsets)
+        if (u < a.n_units && r >= 0) {
+            while (r + 1 < R && a.unit_off[r + 1] <= u) ++r;
+            const int64_t first = a.unit_off[r];
+            const int64_t n = a.unit_off[r + 1] - first;
+            const int64_t local = u - first;
+            if (local >= 0 && local < n) {
+                int64_t k0 = a.start ? (int64_t)a.start[r] : 0;
+                k0 = k0 < 0 ? 0 : (k0 > n ? n : k0);
+                h = (local == 0);
+                if (local >= k0) v = (double)vals[u];
+                rj = r;
+            }
+        }
+        rr[j] = rj;
+        head[j] = h;
+        tagg = combine(tagg, Seg{h, v});
+        run[j] = tagg.v;
+    }
+
+    // ---- block-level exclusive scan of the thread aggregates ----
+    Seg inc = tagg;
+#pragma unroll
+    for (int off = 1; off < kWave; off <<= 1) {
+        const uint32_t f2 = __shfl_up(inc.f, off, kWave);
+        const double v2 = __shfl_up(inc.v, off, kWave);
+        if (lane >= off) inc = combine(Seg{f2, v2}, inc);
+    }
+    if (lane == kWave - 1) s_wave[wave] = inc;
+    __syncthreads();
+    Seg wpre{0u, 0.0};
+    for (int w = 0; w < wave; ++w) wpre = combine(wpre, s_wave[w]);
+    Seg excl;
+    {
+        const uint32_t f2 = __shfl_up(inc.f, 1, kWave);
+        const double v2 = __shfl_up(inc.v, 1, kWave);
+        excl = (lane == 0) ? wpre : combine(wpre, Seg{f2, v2});
+    }
+
+    // ---- publish the tile aggregate, then look back ----
+    if (tid == 0) {
+        Seg total{0u, 0.0};
+        for (int w = 0; w < kScanThreads / kWave; ++w) total = combine(total, s_wave[w]);
+        a.desc[tile].value = total.v;
+        a.desc[tile].head = total.f;
+        __hip_atomic_store(&a.desc[tile].status, 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+
+        double carry = 0.0;
+        const int64_t r0 = s_r0;
+        const bool continues = tile > 0 && r0 >= 0 && a.unit_off[r0] < u0;
+        if (continues) {
+            for (int64_t p = tile - 1; p >= 0; --p) {
+                uint32_t spins = 0;
+                while (__hip_atomic_load(&a.desc[p].status, __ATOMIC_ACQUIRE,
+                                         __HIP_MEMORY_SCOPE_AGENT) == 0u) {
+                    if (++spins > kSpinLimit) break;
+                    __builtin_amdgcn_s_sleep(1);
+                }
+                if (spins > kSpinLimit) {
+                    raise_flag(a.flags, STRIDE_FLAG_SPIN_LIMIT);
+                    carry = __builtin_nan("");
+                    break;
+                }
+                carry = a.desc[p].value + carry;
+                if (a.desc[p].head) break;
+            }
+        }
+        s_carry = carry;
+    }
+    __syncthreads();
+    const double carry = s_carry;
+    const int64_t r0 = s_r0;
+
+    // ---- cumulative values and first crossings ----
+    uint32_t seen = excl.f;
+    int64_t last_r = -2;
+#pragma unroll
+    for (int j = 0; j < kScanItems; ++j) {
+        const int64_t u = ubase + j;
+        if (u >= a.n_units) break;
+        const int64_t rj = rr[j];
+        seen |= head[j];
+        double c;
+        if (rj < 0) {
+            c = __builtin_nan("");
+        } else {
+            // thread-local running sum restarted at a head inside this thread's items
+            bool head_in_thread = false;
+            for (int q = 0; q <= j; ++q) head_in_thread |= (head[q] != 0);
+            c = head_in_thread ? run[j] : excl.v + run[j];
+            if (!seen) c += carry;
+        }
+        a.cum[u] = c;
+        if (rj < 0 || rj == last_r) continue;
+        const int64_t first = a.unit_off[rj];
+        const int64_t local = u - first;
+        int64_t k0 = a.start ? (int64_t)a.start[rj] : 0;
+        const int64_t n = a.unit_off[rj + 1] - first;
+        k0 = k0 < 0 ? 0 : (k0 > n ? n : k0);
+        const int32_t d = a.L.domain ? a.L.domain[rj] : 0;
+        const double lam = (d >= 0 && d < a.n_dom) ? a.lambda.v[d] : __builtin_nan("");
+        if (local >= k0 && c < lam) {
+            last_r = rj;  // later units of this rollout in this thread cannot be earlier
+            const int64_t slot = rj - r0;
+            if (r0 >= 0 && slot >= 0 && slot < kSlots)
+                atomicMin(&s_first[slot], (int32_t)local);
+            else
+                atomicMin(&a.stop_unit[rj], (int32_t)local);
+        }
+    }
+    __syncthreads();
+    if (r0 >= 0) {
+        for (int i = tid; i < kSlots; i += blockDim.x) {
+            if (s_first[i] != INT_MAX) atomicMin(&a.stop_unit[r0 + i], s_first[i]);
+        }
+    }
+}
+
+// stop_unit sentinel -> -1, retained row counts, bad domains.
+__global__ __launch_bounds__(256) void stop_finish_kernel(StopArgs a) {
+    const int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (r >= a.L.n_rollouts) return;
+    const int32_t d = a.L.domain ? a.L.domain[r] : 0;
+    if (d < 0 || d >= a.n_dom) raise_flag(a.flags, STRIDE_FLAG_BAD_DOMAIN);
+    int32_t s = a.stop_unit[r];
+    if (s == INT_MAX) s = -1;
+    a.stop_unit[r] = s;
+    if (!a.retained) return;
+    const int64_t first = a.unit_off[r];
+    int64_t n = a.unit_off[r + 1] - first;
+    if (n < 0) n = 0;
+    int64_t k0 = a.start ? (int64_t)a.start[r] : 0;
+    k0 = k0 < 0 ? 0 : (k0 > n ? n : k0);
+    int64_t end = (s >= 0) ? (int64_t)s + 1 : n;
+    if (end < k0) end = k0;
+    if (a.unit == STRIDE_UNIT_TOKEN) {
+        a.retained[r] = end - k0;
+    } else {
+        const int64_t T = a.L.n_turns;
+        int64_t t0 = first + k0, t1 = first + end;
+        t0 = t0 > T ? T : t0;
+        t1 = t1 > T ? T : t1;
+        a.retained[r] = a.L.turn_tok_off[t1] - a.L.turn_tok_off[t0];
+    }
+}
+
+}  // namespace
+
+hipError_t launch_stop(const stride_layout &L, int32_t unit, const void *values,
+                       const DomainTable &lambda, int32_t n_dom, const int32_t *start,
+                       double *cum, int32_t *stop_unit, int64_t *retained, uint32_t *flags,
+                       void *ws, hipStream_t stream) {
+    const int64_t n_units = (unit == STRIDE_UNIT_TURN) ? L.n_turns : L.n_tokens;
+    const WsLayout w = ws_layout(L.n_rollouts, L.n_tokens, n_units, 0);
+    char *base = static_cast<char *>(ws);
+    StopArgs a;
+    a.L = L;
+    a.lambda = lambda;
+    a.n_dom = n_dom;
+    a.unit = unit;
+    a.n_units = n_units;
+    a.n_tiles = (n_units + kScanTile - 1) / kScanTile;
+    a.values = values;
+    a.start = start;
+    a.unit_off = reinterpret_cast<const int64_t *>(base + w.unit_off);
+    a.cum = cum;
+    a.stop_unit = stop_unit;
+    a.retained = retained;
+    a.counter = reinterpret_cast<uint32_t *>(base + w.counter);
+    a.desc = reinterpret_cast<TileDesc *>(base + w.desc);
+    a.flags = flags;
+
+    const int64_t prep_n = (L.n_rollouts + 1 > a.n_tiles) ? L.n_rollouts + 1 : a.n_tiles;
+    hipLaunchKernelGGL(stop_prep_kernel, dim3((unsigned)((prep_n + 255) / 256)), dim3(256), 0,
+                       stream, a, reinterpret_cast<int64_t *>(base + w.unit_off));
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    if (a.n_tiles > 0) {
+        if (unit == STRIDE_UNIT_TURN)
+            hipLaunchKernelGGL(stop_scan_kernel<double>, dim3((unsigned)a.n_tiles),
+                               dim3(kScanThreads), 0, stream, a);
+        else
+            hipLaunchKernelGGL(stop_scan_kernel<float>, dim3((unsigned)a.n_tiles),
+                               dim3(kScanThreads), 0, stream, a);
+        e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    if (L.n_rollouts > 0) {
+        hipLaunchKernelGGL(stop_finish_kernel, dim3((unsigned)((L.n_rollouts + 255) / 256)),
+                           dim3(256), 0, stream, a);
+        e = hipGetLastError();
+    }
+    return e;
+}
+
+}  // namespace stride

@@ -1,0 +1,278 @@
+// score.hip -- sampled-token log-probabilities of teacher and student rows.
+//
+// Eq. (1) (Sec. 3.1): log pi(y_t | y_<t) = x[y_t] - log sum_v exp(x[v]) over the
+// row's V logits.  Each row is read exactly once from HBM.
+//
+// Design (gfx950, wave64): one wavefront per row; a workgroup holds four
+// independent rows.  Lanes stream the row with 16-byte non-temporal loads
+// (8 bf16 or 4 fp32 per load, consecutive lanes on consecutive 16-byte words,
+// so one wave instruction moves 1 KiB, fully coalesced).  Each lane keeps a
+// running (max m, sum s) in fp32 registers and rescales once per chunk of
+// U loads, not once per element (online normaliser, Milakov and Gimelshein
+// 2018).  Per element the work is: unpack (shift or mask), max, one fma into
+// the exp2 argument, v_exp_f32, add.  The 64 lane states are merged with a
+// fixed butterfly of cross-lane shuffles, so the result does not depend on
+// timing.  The sampled logit is fetched with one scalar-sized load per row.
+#include "common.hpp"
+
+namespace stride {
+namespace {
+
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.69314718055994531f;
+constexpr uint8_t kBadDomain = 0xFF;
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+template <int DT>
+struct Elem;
+template <>
+struct Elem<STRIDE_BF16> {
+    static constexpr int kPerVec = 8;
+    static constexpr int kSize = 2;
+};
+template <>
+struct Elem<STRIDE_F32> {
+    static constexpr int kPerVec = 4;
+    static constexpr int kSize = 4;
+};
+
+template <int DT>
+__device__ __forceinline__ void unpack(const u32x4 &v, float *x);
+
+template <>
+__device__ __forceinline__ void unpack<STRIDE_BF16>(const u32x4 &v, float *x) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        x[2 * i] = __uint_as_float(v[i] << 16);
+        x[2 * i + 1] = __uint_as_float(v[i] & 0xFFFF0000u);
+    }
+}
+
+template <>
+__device__ __forceinline__ void unpack<STRIDE_F32>(const u32x4 &v, float *x) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) x[i] = __uint_as_float(v[i]);
+}
+
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// Fold n values into the lane's running (m, s0 + s1).  The reference point is
+// the running maximum; a state that has only seen -inf keeps reference 0 so
+// that -inf - -inf never appears.
+template <int N>
+__device__ __forceinline__ void fold(float &m, float &s0, float &s1, const float *x) {
+    float cm = x[0];
+#pragma unroll
+    for (int i = 1; i < N; ++i) cm = fmaxf(cm, x[i]);
+    const float mn = fmaxf(m, cm);
+    const float ref = (mn == -INFINITY) ? 0.0f : mn;
+    const float scale = fast_exp2((m - ref) * kLog2e);
+    s0 *= scale;
+    s1 *= scale;
+    const float mref = ref * kLog2e;
+#pragma unroll
+    for (int i = 0; i < N; i += 2) {
+        s0 += fast_exp2(__builtin_fmaf(x[i], kLog2e, -mref));
+        if (i + 1 < N) s1 += fast_exp2(__builtin_fmaf(x[i + 1], kLog2e, -mref));
+    }
+    m = mn;
+}
+
+// Merge two (m, s) states.
+__device__ __forceinline__ void merge(float &m, float &s, float m2, float s2) {
+    const float mn = fmaxf(m, m2);
+    const float ref = (mn == -INFINITY) ? 0.0f : mn;
+    s = s * fast_exp2((m - ref) * kLog2e) + s2 * fast_exp2((m2 - ref) * kLog2e);
+    m = mn;
+}
+
+struct ScoreArgs {
+    PtrTable teachers;
+    const void *student;
+    const uint8_t *row_dom;
+    const int32_t *ids;
+    float *logp_t;
+    float *logp_s;
+    uint32_t *flags;
+    int64_t n_rows;
+    int64_t ld;
+    int32_t vocab;
+    int32_t n_teachers;
+};
+
+template <int DT, int U>
+__global__ __launch_bounds__(256) void score_rows_kernel(ScoreArgs a) {
+    constexpr int E = Elem<DT>::kPerVec;
+    const int lane = threadIdx.x & (kWave - 1);
+    const int64_t item = (int64_t)blockIdx.x * (blockDim.x / kWave) + (threadIdx.x / kWave);
+    const bool two = a.student != nullptr;
+    const int64_t n_items = two ? 2 * a.n_rows : a.n_rows;
+    if (item >= n_items) return;
+    const bool is_student = two && (item & 1);
+    const int64_t row = two ? (item >> 1) : item;
+    float *out = is_student ? a.logp_s : a.logp_t;
+
+    const void *base;
+    if (is_student) {
+        base = a.student;
+    } else {
+        const int d = a.row_dom ? (int)a.row_dom[row] : 0;
+        if (d >= a.n_teachers) {  // row not covered by the layout or bad domain (already flagged)
+            if (lane == 0) out[row] = __builtin_nanf("");
+            return;
+        }
+        base = a.teachers.p[d];
+    }
+    const u32x4 *p = reinterpret_cast<const u32x4 *>(static_cast<const char *>(base) +
+                                                     row * a.ld * Elem<DT>::kSize);
+    const int64_t nvec = a.vocab / E;  // 16-byte words lying wholly inside [0, vocab)
+    const int tail = a.vocab % E;
+
+    float m = -INFINITY, s0 = 0.0f, s1 = 0.0f;
+    int64_t k = 0;
+    constexpr int64_t kStep = (int64_t)U * kWave;
+    for (; k + kStep <= nvec; k += kStep) {
+        u32x4 v[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) v[u] = __builtin_nontemporal_load(p + k + u * kWave + lane);
+        float x[U * E];
+#pragma unroll
+        for (int u = 0; u < U; ++u) unpack<DT>(v[u], x + u * E);
+        fold<U * E>(m, s0, s1, x);
+    }
+    for (; k < nvec; k += kWave) {
+        if (k + lane < nvec) {
+            u32x4 v = __builtin_nontemporal_load(p + k + lane);
+            float x[E];
+            unpack<DT>(v, x);
+            fold<E>(m, s0, s1, x);
+        }
+    }
+    if (tail && lane == 0) {
+        // The last word also holds ld - vocab padding elements: mask them out.
+        u32x4 v = p[nvec];
+        float x[E];
+        unpack<DT>(v, x);
+#pragma unroll
+        for (int j = 0; j < E; ++j)
+            if (j >= tail) x[j] = -INFINITY;
+        fold<E>(m, s0, s1, x);
+    }
+    float s = s0 + s1;
+#pragma unroll
+    for (int off = kWave / 2; off > 0; off >>= 1) {
+        const float m2 = __shfl_xor(m, off, kWave);
+        const float s2 = __shfl_xor(s, off, kWave);
+        merge(m, s, m2, s2);
+    }
+    if (lane == 0) {
+        const int32_t y = a.ids[row];
+        float r;
+        uint32_t bad = 0;
+        const bool finite = (m > -INFINITY) && (m < INFINITY) && (s > 0.0f) && (s < INFINITY);
+        if (!finite) bad |= STRIDE_FLAG_NONFINITE;
+        if (y < 0 || y >= a.vocab) bad |= STRIDE_FLAG_TOKEN_OOB;
+        if (bad) {
+            r = __builtin_nanf("");
+            raise_flag(a.flags, bad);
+        } else {
+            float xy;
+            if (DT == STRIDE_BF16)
+                xy = __uint_as_float((uint32_t)(reinterpret_cast<const uint16_t *>(p)[y]) << 16);
+            else
+                xy = reinterpret_cast<const float *>(p)[y];
+            r = (xy - m) - __builtin_amdgcn_logf(s) * kLn2;
+        }
+        out[row] = r;
+    }
+}
+
+// Teacher index of every row: row -> turn (by offsets) -> rollout -> domain.
+// Rows outside every turn, or whose rollout's domain is out of range, get
+// kBadDomain and raise a flag, so the scoring kernel writes NaN for them.
+__global__ __launch_bounds__(256) void row_domain_kernel(stride_layout L, int32_t n_teachers,
+                                                         uint8_t *row_dom, uint32_t *flags) {
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= L.n_tokens) return;
+    // last turn t with turn_tok_off[t] <= i
+    int64_t lo = 0, hi = L.n_turns;  // answer in [0, T)
+    if (L.n_turns == 0 || L.turn_tok_off[0] > i) {
+        row_dom[i] = kBadDomain;
+        raise_flag(flags, STRIDE_FLAG_BAD_OFFSETS);
+        return;
+    }
+    while (hi - lo > 1) {
+        const int64_t mid = (lo + hi) >> 1;
+        if (L.turn_tok_off[mid] <= i) lo = mid; else hi = mid;
+    }
+    const int64_t t = lo;
+    if (i >= L.turn_tok_off[t + 1]) {
+        row_dom[i] = kBadDomain;
+        raise_flag(flags, STRIDE_FLAG_BAD_OFFSETS);
+        return;
+    }
+    int64_t rlo = 0, rhi = L.n_rollouts;
+    if (L.n_rollouts == 0 || L.rollout_turn_off[0] > t) {
+        row_dom[i] = kBadDomain;
+        raise_flag(flags, STRIDE_FLAG_BAD_OFFSETS);
+        return;
+    }
+    while (rhi - rlo > 1) {
+        const int64_t mid = (rlo + rhi) >> 1;
+        if (L.rollout_turn_off[mid] <= t) rlo = mid; else rhi = mid;
+    }
+    if (t >= L.rollout_turn_off[rlo + 1]) {
+        row_dom[i] = kBadDomain;
+        raise_flag(flags, STRIDE_FLAG_BAD_OFFSETS);
+        return;
+    }
+    const int32_t d = L.domain ? L.domain[rlo] : 0;
+    if (d < 0 || d >= n_teachers) {
+        row_dom[i] = kBadDomain;
+        raise_flag(flags, STRIDE_FLAG_BAD_DOMAIN);
+        return;
+    }
+    row_dom[i] = (uint8_t)d;
+}
+
+}  // namespace
+
+hipError_t launch_row_domain(const stride_layout &L, int32_t n_teachers, uint8_t *row_dom,
+                             uint32_t *flags, hipStream_t stream) {
+    if (L.n_tokens == 0) return hipSuccess;
+    const int64_t blocks = (L.n_tokens + 255) / 256;
+    hipLaunchKernelGGL(row_domain_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, L,
+                       n_teachers, row_dom, flags);
+    return hipGetLastError();
+}
+
+hipError_t launch_score_rows(int32_t dtype, const PtrTable &teachers, int32_t n_teachers,
+                             const uint8_t *row_dom, const void *student, const int32_t *ids,
+                             float *logp_t, float *logp_s, int64_t n_rows, int32_t vocab,
+                             int64_t ld, uint32_t *flags, hipStream_t stream) {
+    if (n_rows == 0) return hipSuccess;
+    ScoreArgs a;
+    a.teachers = teachers;
+    a.student = student;
+    a.row_dom = row_dom;
+    a.ids = ids;
+    a.logp_t = logp_t;
+    a.logp_s = logp_s;
+    a.flags = flags;
+    a.n_rows = n_rows;
+    a.ld = ld;
+    a.vocab = vocab;
+    a.n_teachers = n_teachers;
+    const int64_t items = student ? 2 * n_rows : n_rows;
+    const int64_t blocks = (items + 3) / 4;
+    if (dtype == STRIDE_BF16)
+        hipLaunchKernelGGL((score_rows_kernel<STRIDE_BF16, 8>), dim3((unsigned)blocks), dim3(256), 0,
+                           stream, a);
+    else
+        hipLaunchKernelGGL((score_rows_kernel<STRIDE_F32, 8>), dim3((unsigned)blocks), dim3(256), 0,
+                           stream, a);
+    return hipGetLastError();
+}
+
+}  // namespace stride

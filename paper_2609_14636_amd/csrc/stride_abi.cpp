@@ -1,0 +1,223 @@
+// stride_abi.cpp -- the extern "C" entry points of libstride.so.
+//
+// Host-side argument checking (synchronous, before any launch), workspace
+// carving and the launch sequence of each call.  Every launch is asynchronous
+// on the caller's stream; nothing here synchronises or allocates.
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+
+#include "common.hpp"
+
+namespace stride {
+
+static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+WsLayout ws_layout(int64_t n_rollouts, int64_t n_tokens, int64_t n_units, int64_t fused_partials) {
+    WsLayout w;
+    size_t off = 0;
+    w.counter = off;
+    off += 256;
+    w.row_dom = off;
+    off += align256((size_t)(n_tokens > 0 ? n_tokens : 0));
+    w.unit_off = off;
+    off += align256(sizeof(int64_t) * (size_t)(n_rollouts + 1));
+    w.desc = off;
+    const int64_t tiles = n_units > 0 ? (n_units + kScanTile - 1) / kScanTile : 0;
+    off += align256(sizeof(TileDesc) * (size_t)tiles);
+    w.fused = off;
+    off += align256(8 * (size_t)(fused_partials > 0 ? fused_partials : 0));
+    w.total = off;
+    return w;
+}
+
+}  // namespace stride
+
+using namespace stride;
+
+namespace {
+
+thread_local char g_err[512] = "";
+
+stride_status fail(stride_status st, const char *fmt, ...) {
+    va_list ap;
+    va_start(ap, fmt);
+    std::vsnprintf(g_err, sizeof g_err, fmt, ap);
+    va_end(ap);
+    return st;
+}
+
+stride_status ok() {
+    g_err[0] = '\0';
+    return STRIDE_OK;
+}
+
+bool aligned(const void *p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+stride_status check_layout(const stride_layout *L) {
+    if (!L) return fail(STRIDE_ERR_INVALID_ARG, "layout is NULL");
+    if (L->n_rollouts < 0 || L->n_turns < 0 || L->n_tokens < 0)
+        return fail(STRIDE_ERR_INVALID_ARG, "negative layout size (R=%d T=%d N=%lld)", L->n_rollouts,
+                    L->n_turns, (long long)L->n_tokens);
+    if (!L->rollout_turn_off) return fail(STRIDE_ERR_INVALID_ARG, "rollout_turn_off is NULL");
+    if (!L->turn_tok_off) return fail(STRIDE_ERR_INVALID_ARG, "turn_tok_off is NULL");
+    if (L->n_tokens > 0 && L->n_turns == 0)
+        return fail(STRIDE_ERR_INVALID_ARG, "N = %lld rows but no turns", (long long)L->n_tokens);
+    if (L->n_turns > 0 && L->n_rollouts == 0)
+        return fail(STRIDE_ERR_INVALID_ARG, "T = %d turns but no rollouts", L->n_turns);
+    return STRIDE_OK;
+}
+
+stride_status check_ws(const stride_layout *L, int64_t n_units, void *ws, size_t ws_bytes) {
+    const WsLayout w = ws_layout(L->n_rollouts, L->n_tokens, n_units, 0);
+    if (!ws) return fail(STRIDE_ERR_WORKSPACE, "workspace is NULL (need %zu bytes)", w.total);
+    if (!aligned(ws, 256)) return fail(STRIDE_ERR_WORKSPACE, "workspace is not 256-byte aligned");
+    if (ws_bytes < w.total)
+        return fail(STRIDE_ERR_WORKSPACE, "workspace has %zu bytes, need %zu", ws_bytes, w.total);
+    return STRIDE_OK;
+}
+
+stride_status check_domains(const double *table, int32_t n_dom, const char *name) {
+    if (!table) return fail(STRIDE_ERR_INVALID_ARG, "%s is NULL", name);
+    if (n_dom < 1 || n_dom > STRIDE_MAX_DOMAINS)
+        return fail(STRIDE_ERR_UNSUPPORTED, "n_dom = %d outside 1..%d", n_dom, STRIDE_MAX_DOMAINS);
+    return STRIDE_OK;
+}
+
+stride_status hip_fail(hipError_t e, const char *what) {
+    return fail(STRIDE_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t stride_workspace_size(const stride_layout *layout, int32_t unit) {
+    if (!layout) return 0;
+    const int64_t n_units = (unit == STRIDE_UNIT_TOKEN) ? layout->n_tokens : layout->n_turns;
+    return ws_layout(layout->n_rollouts, layout->n_tokens, n_units, 0).total;
+}
+
+const char *stride_last_error(void) { return g_err; }
+
+stride_status stride_score(const stride_layout *layout, int32_t vocab, int64_t ld, int32_t dtype,
+                           int32_t n_teachers, const void *const *teacher_logits,
+                           const void *student_logits, const int32_t *token_ids, float *logp_t,
+                           float *logp_s, float *kl, double *turn_mean, uint32_t *dev_flags,
+                           void *ws, size_t ws_bytes, hipStream_t stream) {
+    stride_status st = check_layout(layout);
+    if (st != STRIDE_OK) return st;
+    const stride_layout &L = *layout;
+    if (vocab < 1) return fail(STRIDE_ERR_INVALID_ARG, "vocab = %d < 1", vocab);
+    if (ld < vocab) return fail(STRIDE_ERR_INVALID_ARG, "ld = %lld < vocab = %d", (long long)ld, vocab);
+    if (dtype != STRIDE_BF16 && dtype != STRIDE_F32)
+        return fail(STRIDE_ERR_UNSUPPORTED, "dtype %d is neither STRIDE_BF16 nor STRIDE_F32", dtype);
+    const int64_t esize = dtype == STRIDE_BF16 ? 2 : 4;
+    if ((ld * esize) % 16 != 0)
+        return fail(STRIDE_ERR_UNSUPPORTED, "row stride %lld bytes is not a multiple of 16",
+                    (long long)(ld * esize));
+    if (n_teachers < 1 || n_teachers > STRIDE_MAX_DOMAINS)
+        return fail(STRIDE_ERR_UNSUPPORTED, "n_teachers = %d outside 1..%d", n_teachers,
+                    STRIDE_MAX_DOMAINS);
+    if (!student_logits && (logp_s || kl))
+        return fail(STRIDE_ERR_INVALID_ARG, "logp_s / kl requested without student logits");
+    if (L.n_tokens > 0) {
+        if (!teacher_logits) return fail(STRIDE_ERR_INVALID_ARG, "teacher_logits is NULL");
+        for (int d = 0; d < n_teachers; ++d) {
+            if (!teacher_logits[d])
+                return fail(STRIDE_ERR_INVALID_ARG, "teacher_logits[%d] is NULL", d);
+            if (!aligned(teacher_logits[d], 16))
+                return fail(STRIDE_ERR_UNSUPPORTED, "teacher_logits[%d] is not 16-byte aligned", d);
+        }
+        if (student_logits && !aligned(student_logits, 16))
+            return fail(STRIDE_ERR_UNSUPPORTED, "student_logits is not 16-byte aligned");
+        if (!token_ids) return fail(STRIDE_ERR_INVALID_ARG, "token_ids is NULL");
+        if (!logp_t) return fail(STRIDE_ERR_INVALID_ARG, "logp_t is NULL");
+    }
+    if (L.n_turns > 0 && !turn_mean) return fail(STRIDE_ERR_INVALID_ARG, "turn_mean is NULL");
+    const bool routed = n_teachers > 1 && L.domain != nullptr;
+    if (routed) {
+        st = check_ws(layout, 0, ws, ws_bytes);
+        if (st != STRIDE_OK) return st;
+    }
+
+    PtrTable tp{};
+    for (int d = 0; d < n_teachers && teacher_logits; ++d) tp.p[d] = teacher_logits[d];
+    uint8_t *row_dom = nullptr;
+    hipError_t e;
+    if (routed && L.n_tokens > 0) {
+        const WsLayout w = ws_layout(L.n_rollouts, L.n_tokens, 0, 0);
+        row_dom = static_cast<uint8_t *>(ws) + w.row_dom;
+        e = launch_row_domain(L, n_teachers, row_dom, dev_flags, stream);
+        if (e != hipSuccess) return hip_fail(e, "row-domain launch");
+    }
+    e = launch_score_rows(dtype, tp, n_teachers, row_dom, student_logits, token_ids, logp_t,
+                          logp_s, L.n_tokens, vocab, ld, dev_flags, stream);
+    if (e != hipSuccess) return hip_fail(e, "row-scoring launch");
+    e = launch_turn_mean(L, logp_t, logp_s, kl, turn_mean, dev_flags, stream);
+    if (e != hipSuccess) return hip_fail(e, "turn-mean launch");
+    return ok();
+}
+
+stride_status stride_score_fused(const stride_layout *layout, int32_t vocab, int32_t d,
+                                 const void *hidden_t, const void *w_t, const void *student_logits,
+                                 int64_t ld, const int32_t *token_ids, float *logp_t, float *logp_s,
+                                 float *kl, double *turn_mean, uint32_t *dev_flags, void *ws,
+                                 size_t ws_bytes, hipStream_t stream) {
+    (void)layout; (void)vocab; (void)d; (void)hidden_t; (void)w_t; (void)student_logits; (void)ld;
+    (void)token_ids; (void)logp_t; (void)logp_s; (void)kl; (void)turn_mean; (void)dev_flags;
+    (void)ws; (void)ws_bytes; (void)stream;
+    return fail(STRIDE_ERR_UNSUPPORTED, "stride_score_fused is not available in this build");
+}
+
+stride_status stride_stop(const stride_layout *layout, int32_t unit, const void *values,
+                          const double *lambda, int32_t n_dom, const int32_t *start_unit,
+                          double *cum, int32_t *stop_unit, int64_t *n_retained_tokens,
+                          uint32_t *dev_flags, void *ws, size_t ws_bytes, hipStream_t stream) {
+    stride_status st = check_layout(layout);
+    if (st != STRIDE_OK) return st;
+    const stride_layout &L = *layout;
+    if (unit != STRIDE_UNIT_TURN && unit != STRIDE_UNIT_TOKEN)
+        return fail(STRIDE_ERR_INVALID_ARG, "unit %d is neither STRIDE_UNIT_TURN nor STRIDE_UNIT_TOKEN",
+                    unit);
+    st = check_domains(lambda, n_dom, "lambda");
+    if (st != STRIDE_OK) return st;
+    const int64_t n_units = (unit == STRIDE_UNIT_TURN) ? L.n_turns : L.n_tokens;
+    if (n_units > 0 && (!values || !cum))
+        return fail(STRIDE_ERR_INVALID_ARG, "values or cum is NULL");
+    if (L.n_rollouts > 0 && !stop_unit) return fail(STRIDE_ERR_INVALID_ARG, "stop_unit is NULL");
+    st = check_ws(layout, n_units, ws, ws_bytes);
+    if (st != STRIDE_OK) return st;
+    DomainTable lt{};
+    for (int i = 0; i < n_dom; ++i) lt.v[i] = lambda[i];
+    const hipError_t e = launch_stop(L, unit, values, lt, n_dom, start_unit, cum, stop_unit,
+                                     n_retained_tokens, dev_flags, ws, stream);
+    if (e != hipSuccess) return hip_fail(e, "stop launch");
+    return ok();
+}
+
+stride_status stride_restart_turn(const stride_layout *layout, int32_t unit, const void *values,
+                                  const int32_t *stop_unit, const double *alpha, int32_t n_dom,
+                                  const uint8_t *correct_mask, int32_t *k_star, int32_t *k0,
+                                  int32_t *k_max, uint32_t *dev_flags, hipStream_t stream) {
+    stride_status st = check_layout(layout);
+    if (st != STRIDE_OK) return st;
+    const stride_layout &L = *layout;
+    if (unit != STRIDE_UNIT_TURN && unit != STRIDE_UNIT_TOKEN)
+        return fail(STRIDE_ERR_INVALID_ARG, "unit %d is neither STRIDE_UNIT_TURN nor STRIDE_UNIT_TOKEN",
+                    unit);
+    st = check_domains(alpha, n_dom, "alpha");
+    if (st != STRIDE_OK) return st;
+    const int64_t n_units = (unit == STRIDE_UNIT_TURN) ? L.n_turns : L.n_tokens;
+    if (n_units > 0 && !values) return fail(STRIDE_ERR_INVALID_ARG, "values is NULL");
+    if (L.n_rollouts > 0 && (!k_star || !k0))
+        return fail(STRIDE_ERR_INVALID_ARG, "k_star or k0 is NULL");
+    DomainTable at{};
+    for (int i = 0; i < n_dom; ++i) at.v[i] = alpha[i];
+    const hipError_t e = launch_restart(L, unit, values, stop_unit, at, n_dom, correct_mask, k_star,
+                                        k0, k_max, dev_flags, stream);
+    if (e != hipSuccess) return hip_fail(e, "restart launch");
+    return ok();
+}
+
+}  // extern "C"

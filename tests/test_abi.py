@@ -1,0 +1,110 @@
+"""The C ABI on the CPU: the library loads, exports what include/stride.h declares, and rejects
+bad arguments on the host before launching anything (no call here reaches a kernel)."""
+import ctypes
+import os
+import re
+
+import pytest
+import torch
+
+import paper_2609_14636_amd as P
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def declared_functions():
+    names = []
+    for fn in os.listdir(os.path.join(ROOT, "include")):
+        if fn.endswith(".h"):
+            text = open(os.path.join(ROOT, "include", fn)).read()
+            text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+            names += re.findall(r"\b(stride_[a-z_]+)\s*\(", text)
+    return sorted(set(names))
+
+
+def test_every_declared_symbol_is_exported():
+    names = declared_functions()
+    assert {"stride_score", "stride_stop", "stride_restart_turn", "stride_score_fused",
+            "stride_workspace_size", "stride_last_error"} <= set(names)
+    lib = ctypes.CDLL(P.stride.LIB_PATH)
+    for n in names:
+        assert hasattr(lib, n), f"{n} is declared but not exported"
+
+
+def test_header_compiles_as_c():
+    import subprocess
+    src = '#include "stride.h"\nint main(void){ return (int)sizeof(stride_layout); }\n'
+    r = subprocess.run(["gcc", "-std=c99", "-fsyntax-only", "-I", os.path.join(ROOT, "include"),
+                        "-I", "/opt/rocm/include", "-D__HIP_PLATFORM_AMD__", "-x", "c", "-"],
+                       input=src, capture_output=True, text=True)
+    assert r.returncode == 0, r.stderr
+
+
+def _layout(R=2, T=3, N=10):
+    rto = torch.tensor([0, 2, 3][:R + 1], dtype=torch.int32)
+    tto = torch.tensor([0, 4, 7, N][:T + 1], dtype=torch.int64)
+    return P.Layout(rto, tto, N)
+
+
+def test_workspace_size():
+    lay = _layout()
+    a = P.stride_workspace_size(lay, P.STRIDE_UNIT_TURN)
+    b = P.stride_workspace_size(lay, P.STRIDE_UNIT_TOKEN)
+    assert a > 0 and b >= a and a % 256 == 0
+    big = P.Layout(torch.zeros(9, dtype=torch.int32), torch.zeros(2, dtype=torch.int64), 10**6)
+    assert P.stride_workspace_size(big, P.STRIDE_UNIT_TOKEN) >= 10**6
+
+
+def _fake(n):
+    """A CPU tensor standing in for a device buffer; only calls that fail validation use it."""
+    return torch.zeros(n, dtype=torch.float32)
+
+
+@pytest.mark.parametrize("case,status", [
+    ("vocab0", P.stride.StrideError), ("ld_small", P.stride.StrideError),
+    ("bad_unit", P.stride.StrideError), ("ws_small", P.stride.StrideError),
+    ("n_dom0", P.stride.StrideError), ("kl_without_student", P.stride.StrideError),
+])
+def test_argument_errors_raise_before_launch(case, status):
+    lay = _layout()
+    x = torch.zeros((10, 16), dtype=torch.float32)
+    ids = torch.zeros(10, dtype=torch.int32)
+    out = _fake(10)
+    tm = torch.zeros(3, dtype=torch.float64)
+    ws = torch.zeros(P.stride_workspace_size(lay, P.STRIDE_UNIT_TOKEN), dtype=torch.uint8)
+    with pytest.raises(status) as ei:
+        if case == "vocab0":
+            P.stride_score(lay, 0, [x], x, ids, out, out, out, tm, None, ws, stream=0)
+        elif case == "ld_small":
+            P.stride_score(lay, 17, [x], x, ids, out, out, out, tm, None, ws, stream=0)
+        elif case == "bad_unit":
+            P.stride_stop(lay, 9, tm, [-1.0], None, tm, ids, None, None, ws, stream=0)
+        elif case == "ws_small":
+            P.stride_stop(lay, P.STRIDE_UNIT_TOKEN, out, [-1.0], None, tm, ids, None, None,
+                          ws[:100], stream=0)
+        elif case == "n_dom0":
+            P.stride_restart_turn(lay, P.STRIDE_UNIT_TURN, tm, None, [], None, ids, ids, None,
+                                  None, stream=0)
+        elif case == "kl_without_student":
+            P.stride_score(lay, 16, [x], None, ids, out, None, out, tm, None, ws, stream=0)
+    assert ei.value.status in (1, 2, 3)
+    assert P.library().stride_last_error().decode()
+
+
+def test_unaligned_row_stride_is_unsupported():
+    lay = _layout()
+    x = torch.zeros((10, 15), dtype=torch.bfloat16)  # 30-byte rows
+    ids = torch.zeros(10, dtype=torch.int32)
+    with pytest.raises(P.StrideError) as ei:
+        P.stride_score(lay, 15, [x], None, ids, _fake(10), None, None,
+                       torch.zeros(3, dtype=torch.float64), None, None, stream=0)
+    assert ei.value.status == 2
+
+
+def test_fused_variant_reports_its_status():
+    lay = _layout()
+    with pytest.raises(P.StrideError):
+        P.library().stride_score_fused  # exported
+        st = P.library().stride_score_fused(None, 0, 0, None, None, None, 0, None, None, None,
+                                            None, None, None, None, 0, None)
+        P.stride._check(st)
