@@ -47,9 +47,12 @@ def source_digest() -> str:
         return hashlib.sha256(f.read()).hexdigest()[:16]
 
 
-def measured_traffic(workload: str, bytes_alg: float):
+def measured_traffic(workload: str):
     """HBM bytes per launch of the scoring kernel from committed rocprofv3 counters, if they were
-    taken on the current kernel source; else None."""
+    taken on the current kernel source; else None.
+
+    FETCH_SIZE and WRITE_SIZE (KiB per dispatch) are each scaled by the ratio of known bytes to
+    the same counter's reading on a one-dispatch plain copy (torch.neg on float32)."""
     if not os.path.exists(TRAFFIC):
         return None
     with open(TRAFFIC) as f:
@@ -57,23 +60,23 @@ def measured_traffic(workload: str, bytes_alg: float):
     e = t.get(workload)
     if not e or e.get("score_hip_sha256_16") != source_digest():
         return None
-    return float(e["bytes_per_launch"])
+    c = t["copy_calibration"]
+    k_fetch = c["bytes"] / (c["fetch_kib"] * 1024.0)
+    k_write = c["bytes"] / (c["write_kib"] * 1024.0)
+    return e["fetch_kib"] * 1024.0 * k_fetch + e["write_kib"] * 1024.0 * k_write
 
 
-def cpu_baseline(wl, lam, alpha, budget_rows: int):
-    """Float64 oracle on whole rollouts of the workload (at least one), compute time only."""
+def cpu_baseline(wl, lam, alpha, budget_s: float):
+    """Float64 oracle on whole rollouts of the workload, in order, until budget_s seconds of
+    oracle compute (at least one rollout); compute time only, host input generation excluded."""
     from tests import harness as H
 
     threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
     rows, rs = 0, []
-    for r in range(wl.n_rollouts):
-        a, b = wl.rollout_rows(r)
-        if rs and rows + (b - a) > budget_rows:
-            break
-        rs.append(r)
-        rows += b - a
     t_gen, t_ora = 0.0, 0.0
-    for r in rs:
+    for r in range(wl.n_rollouts):
+        if rs and t_ora >= budget_s:
+            break
         a, b = wl.rollout_rows(r)
         t0 = time.perf_counter()
         t = wl.teacher_rows_host(a, b - a, threads)
@@ -85,10 +88,13 @@ def cpu_baseline(wl, lam, alpha, budget_rows: int):
         del t, s
         t_gen += t1 - t0
         t_ora += t2 - t1
+        rs.append(r)
+        rows += b - a
     return {"value": rows / t_ora, "unit": "tokens/s", "cores": threads, "kind": "oracle",
-            "sample": f"rollouts {rs[0]}..{rs[-1]} of the timed workload ({rows} tokens, "
-                      f"{2 * rows} logit rows of V={wl.vocab}); oracle compute {t_ora:.1f} s, "
-                      f"input generation {t_gen:.1f} s not counted"}
+            "sample": f"rollouts {rs[0]}..{rs[-1]} of {wl.n_rollouts} of the timed workload "
+                      f"({rows} tokens = {2 * rows} logit rows of V={wl.vocab}, whole path per "
+                      f"rollout); oracle compute {t_ora:.1f} s, host input generation "
+                      f"{t_gen:.1f} s not counted"}
 
 
 def main():
@@ -99,9 +105,14 @@ def main():
     ap.add_argument("--workload", default="agentic",
                     choices=["tiny", "agentic", "reasoning", "multi"])
     ap.add_argument("--seed", type=int, default=1001)
-    ap.add_argument("--cpu-rows", type=int, default=6000,
-                    help="bound on the oracle sample (token rows; whole rollouts, at least one)")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0,
+                    help="bound on the oracle sample: whole rollouts are added until the oracle "
+                         "has computed this long (at least one rollout)")
     ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
+                    help="only run a plain elementwise copy (torch.neg on float32) reading and "
+                         "writing BYTES each per dispatch, to calibrate the HBM byte counters; keep "
+                         "BYTES <= 1 GiB so that torch issues one dispatch per copy")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only: --gpus {args.gpus} is not supported "
@@ -109,6 +120,19 @@ def main():
         sys.exit(2)
 
     import torch
+
+    if args.copy_calibration:
+        if args.copy_calibration > 1 << 30:
+            raise SystemExit("--copy-calibration above 1 GiB is split into several dispatches")
+        n = args.copy_calibration // 4
+        src = torch.ones(n, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        for _ in range(3):
+            torch.neg(src, out=dst)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_calibration_bytes": 4 * n, "launches": 3}), flush=True)
+        return
 
     import paper_2609_14636_amd as P
     from synth import workloads as W
@@ -159,7 +183,7 @@ def main():
     per_token = 2 * wl.vocab * wl.esize + 4 + 8  # two logit rows in, token id in, two logps out
     bytes_alg = per_token * n_tok
     achieved = bytes_alg / (score_ms * 1e-3) / 1e9
-    traffic = measured_traffic(args.workload, bytes_alg)
+    traffic = measured_traffic(args.workload)
     res = {
         "metric": METRIC,
         "value": n_tok / (ms_step * 1e-3),
@@ -184,7 +208,7 @@ def main():
     }
     if not args.no_cpu:
         log("[bench] timing the float64 oracle on a bounded sample")
-        res["cpu_baseline"] = cpu_baseline(wl, lam, alpha, args.cpu_rows)
+        res["cpu_baseline"] = cpu_baseline(wl, lam, alpha, args.cpu_seconds)
     print(json.dumps(res), flush=True)
 
 

@@ -65,10 +65,18 @@ def main():
             lam, alpha = WP.reasoning_thresholds(lp, wl.unit_off())
         dom = np.zeros(wl.n_rollouts, np.int64) if wl.domain is None else wl.domain
         vals = tm if wl.unit == W.UNIT_TURN else lp
-        _, stop, _ = O.stop(wl.unit_off(), vals, np.array(lam)[dom])
+        uoff = wl.unit_off()
+        cum, stop, _ = O.stop(uoff, vals, np.array(lam)[dom])
+        rec = np.where(stop >= 0, stop + 1, np.diff(uoff)).astype(np.int32)
+        ks, k0, km = O.restart(uoff, vals, rec, np.array(alpha)[dom], wl.mask)
+        # distance of each rollout's cumulative values to its lambda, for the 1e-3 band rule
+        gap = [float(np.min(np.abs(cum[uoff[r]:uoff[r + 1]] - lam[dom[r]]))) for r in range(wl.n_rollouts)]
         res["workloads"][f"{name}:{seed}"] = {
             "lambda": lam, "alpha": [a if math.isfinite(a) else "-inf" for a in alpha],
-            "oracle_stop": stop.tolist(), "seconds": round(time.time() - t0, 1)}
+            "oracle_stop": stop.tolist(), "oracle_k_star": ks.tolist(), "oracle_k0": k0.tolist(),
+            "oracle_k_max": km.tolist(), "oracle_min_gap_to_lambda": gap,
+            "oracle_turn_mean": tm.tolist() if wl.unit == W.UNIT_TURN else None,
+            "seconds": round(time.time() - t0, 1)}
         print(name, lam, alpha, stop.tolist(), f"{time.time() - t0:.1f}s", flush=True)
         with open(OUT, "w") as f:
             json.dump(res, f, indent=1)
