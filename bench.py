@@ -18,10 +18,13 @@ import os
 import sys
 import time
 
+import numpy as np
+
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
+MFMA_BF16_PEAK_TFLOPS = 2500.0
 METRIC = "scored tokens/sec (logp+KL+stop scan) and % of HBM peak, 1 MI355X"
 PARAMS = os.path.join(ROOT, "tests", "golden", "workload_params.json")
 TRAFFIC = os.path.join(ROOT, "profiles", "traffic.json")
@@ -97,13 +100,108 @@ def cpu_baseline(wl, lam, alpha, budget_s: float):
                       f"{t_gen:.1f} s not counted"}
 
 
+def cpu_baseline_fused(wl, budget_s: float):
+    """Float64 oracle on rows of the fused workload (teacher projection in binary64 plus the
+    student row), batches of 16 rows until budget_s seconds of oracle compute."""
+    from tests import harness as H
+
+    threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+    w_dv = np.ascontiguousarray(wl.w_host(threads).T)
+    rows, t_ora, r0 = 0, 0.0, 0
+    while rows == 0 or (t_ora < budget_s and r0 < wl.n_tokens):
+        idx = np.arange(r0, min(r0 + 16, wl.n_tokens))
+        h = wl.hidden_host(int(idx[0]), idx.size, threads)
+        st = wl.student_rows_host(int(idx[0]), idx.size, threads)
+        t0 = time.perf_counter()
+        H.OP.O.fused_logp(h, w_dv, wl.tok[idx])
+        H.OP.O.logp_rows(st, wl.tok[idx], wl.vocab)
+        t_ora += time.perf_counter() - t0
+        rows += idx.size
+        r0 += idx.size
+    return {"value": rows / t_ora, "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "sample": f"rows 0..{rows - 1} of the timed workload (teacher logits h W formed in "
+                      f"binary64 over d={wl.fused_d}, V={wl.vocab}, plus the student row); "
+                      f"oracle compute {t_ora:.1f} s"}
+
+
+def bench_fused(args):
+    import torch
+
+    import paper_2609_14636_amd as P
+    from synth import workloads as W
+    from tests import harness as H
+    from tests import workload_params as WP
+
+    wl = W.make("fused", seed=args.seed)
+    lam, alpha = WP.fused_thresholds(wl.vocab, wl.fused_d, wl.hidden_sigma, wl.w_sigma)
+    log(f"[bench] workload fused seed {args.seed}: N={wl.n_tokens} d={wl.fused_d} V={wl.vocab}")
+    inp = H.device_inputs_fused(wl)
+    path = P.Path(inp["layout"], wl.unit, with_student=True, fused_vocab=wl.vocab)
+    stream = torch.cuda.current_stream()
+    torch.cuda.synchronize()
+
+    def step():
+        path.score_fused(wl.vocab, inp["hidden"], inp["w"], inp["student"], inp["ids"])
+        path.stop(lam)
+        path.restart(alpha)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    ms_step = (time.perf_counter() - t0) * 1e3 / args.steps
+    out = path.host()
+    if out["flags"] != 0:
+        raise SystemExit(f"device flags {out['flags']:#x} on the benchmark workload")
+    H.assert_invariants(out, wl)
+    # the dominant kernel alone: teacher-only calls (projection + LSE, plus the
+    # per-row gather and merge kernels, <1% of the time)
+    lt = torch.empty_like(path.logp_t)
+    tm = torch.empty_like(path.turn_mean)
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(max(args.steps // 2, 3))]
+    for a, b in ev:
+        a.record(stream)
+        P.stride_score_fused(inp["layout"], wl.vocab, inp["hidden"], inp["w"], None, inp["ids"],
+                             lt, None, None, tm, path.flags, path.fused_ws)
+        b.record(stream)
+    torch.cuda.synchronize()
+    k_ms = sum(a.elapsed_time(b) for a, b in ev) / len(ev)
+    flops = 2.0 * wl.n_tokens * wl.fused_d * wl.vocab
+    achieved = flops / (k_ms * 1e-3) / 1e12
+    log(f"[bench] {args.steps} steps: {ms_step:.3f} ms/step; teacher projection {k_ms:.3f} ms "
+        f"= {achieved:.0f} TFLOP/s")
+    res = {
+        "metric": METRIC, "value": wl.n_tokens / (ms_step * 1e-3), "unit": "tokens/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_step,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": f"fused: {wl.n_rollouts} rollouts x {wl.n_turns} turns, "
+                               f"{wl.n_tokens} scored tokens, teacher logits h W on the fly "
+                               f"(d={wl.fused_d}, V={wl.vocab}), student logits bf16",
+                   "global_batch": wl.n_rollouts, "seq_len": wl.n_tokens // wl.n_rollouts,
+                   "parallelism": "single GPU"},
+        "roofline": {"bound": "mfma", "achieved": achieved, "peak": MFMA_BF16_PEAK_TFLOPS,
+                     "unit": "TFLOP/s", "frac": achieved / MFMA_BF16_PEAK_TFLOPS, "traffic": None,
+                     "kernel": "fused_lse_kernel (bf16 MFMA 32x32x16)", "kernel_ms": k_ms,
+                     "flops_per_launch": flops},
+    }
+    if not args.no_cpu:
+        log("[bench] timing the float64 oracle on a bounded sample")
+        res["cpu_baseline"] = cpu_baseline_fused(wl, args.cpu_seconds)
+    print(json.dumps(res), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="agentic",
-                    choices=["tiny", "agentic", "reasoning", "multi"])
+                    choices=["tiny", "agentic", "reasoning", "multi", "fused"])
     ap.add_argument("--seed", type=int, default=1001)
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="bound on the oracle sample: whole rollouts are added until the oracle "
@@ -139,6 +237,8 @@ def main():
     from tests import harness as H
 
     torch.cuda.set_device(0)
+    if args.workload == "fused":
+        return bench_fused(args)
     wl = W.make(args.workload, seed=args.seed)
     lam, alpha = workload_params(args.workload, args.seed)
     log(f"[bench] workload {args.workload} seed {args.seed}: R={wl.n_rollouts} T={wl.n_turns} "

@@ -117,21 +117,31 @@ stride_status stride_score(const stride_layout *layout, int32_t vocab, int64_t l
 
 /*
  * As stride_score, with the teacher's logits produced by its output
- * projection inside the kernel and never written to memory: z = h W with h
- * the teacher's final hidden state of the row and W its lm_head, followed by
- * the same log-softmax at the sampled token (Eq. 1).  The student's logits
+ * projection inside the kernel and never written to memory: z = h W^T with h
+ * the teacher's final hidden state of the row and W its lm_head weight, then
+ * the same log-softmax at the sampled token (Eq. 1).  The projection runs on
+ * the matrix cores (bf16 inputs, fp32 accumulation).  The student's logits
  * are given as in stride_score.
  *
- *   d                hidden size, a multiple of 64
- *   hidden_t         [N, d] bf16 row-major
- *   w_t              [d, vocab] bf16 row-major (ld of W = vocab, a multiple of 8)
- *   student_logits   [N, ld] bf16 or NULL
+ *   d                hidden size, a positive multiple of 64
+ *   hidden_t         [N, d] bf16 row-major, 16-byte aligned
+ *   w_t              [vocab, d] bf16 row-major (a linear layer's weight: row v
+ *                    holds the weights of vocabulary entry v), 16-byte aligned
+ *   student_logits   [N, ld] bf16 or NULL (as in stride_score)
+ *   ws               at least stride_fused_workspace_size(layout, vocab) bytes
  */
 stride_status stride_score_fused(const stride_layout *layout, int32_t vocab, int32_t d,
                                  const void *hidden_t, const void *w_t, const void *student_logits,
                                  int64_t ld, const int32_t *token_ids, float *logp_t, float *logp_s,
                                  float *kl, double *turn_mean, uint32_t *dev_flags, void *ws,
                                  size_t ws_bytes, hipStream_t stream);
+
+/*
+ * Bytes of workspace stride_score_fused needs: a table of per-row partial
+ * (max, sum) pairs, one per 128 vocabulary entries, plus one float per row.
+ * Host-only; 0 for a NULL layout.
+ */
+size_t stride_fused_workspace_size(const stride_layout *layout, int32_t vocab);
 
 /*
  * Early-stop test, Eq. (5) (Sec. 4.1), over the new units of each rollout:

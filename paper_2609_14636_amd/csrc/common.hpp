@@ -66,6 +66,12 @@ hipError_t launch_stop(const stride_layout &L, int32_t unit, const void *values,
                        double *cum, int32_t *stop_unit, int64_t *retained, uint32_t *flags,
                        void *ws, hipStream_t stream);
 
+// fused.hip
+size_t fused_ws_bytes(int64_t n_rows, int32_t vocab);
+hipError_t launch_fused_teacher(const uint16_t *h, const uint16_t *w, const int32_t *ids,
+                                float *logp_t, int64_t n_rows, int32_t vocab, int32_t d,
+                                uint32_t *flags, void *ws, hipStream_t stream);
+
 // restart.hip
 hipError_t launch_restart(const stride_layout &L, int32_t unit, const void *values,
                           const int32_t *stop_unit, const DomainTable &alpha, int32_t n_dom,

@@ -1,0 +1,271 @@
+// fused.hip -- teacher log-probabilities from the output projection, logits never stored.
+//
+// Eq. (1) (Sec. 3.1) with the teacher's logits z = h W^T, h the teacher's final
+// hidden state of the row ([N, d] bf16) and W its lm_head weight as stored by a
+// linear layer ([V, d] bf16, row v = the weights of vocabulary entry v):
+// log pi_T(y) = z_y - log sum_v exp(z_v).  The [N, V] logits (40 GB at the
+// fused workload) exist only tile by tile in registers.
+//
+// Kernel 1 (MFMA): a 256 x 256 tile of z per workgroup, K = d streamed in
+//   64-wide blocks through double-buffered LDS (rows padded by 16 B), four
+//   waves in a 2 x 2 grid each holding a 128 x 128 fp32 accumulator (16
+//   v_mfma_f32_32x32x16_bf16 tiles).  Both operands are K-contiguous, so each
+//   MFMA operand is one 16-byte LDS read.  The epilogue reduces every row of
+//   each wave's 128 columns to (max, sum of exp(z - max)) with a 32-lane
+//   butterfly and writes it to a partial table [V/128][N] (rows contiguous).
+//   Workgroups are numbered so that the 32 resident on one XCD (dispatch is
+//   round-robin over the 8 XCDs) cover a 4 x 8 block of tiles of a 16 x 16
+//   super-tile, and super-tiles advance along V: each XCD's L2 serves every
+//   H panel slice to 8 tiles and every W slice to 4, and the 16 H panels of a
+//   super-row stay in the last-level cache while W streams past.
+// Kernel 2: z_y = h . w_y per row (one wave per row, fp32).
+// Kernel 3: one thread per row merges its V/128 partials (reads coalesced
+//   across rows) and writes log pi_T(y) = (z_y - m) - log s.
+#include "common.hpp"
+
+namespace stride {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int kBM = 256, kBN = 256, kBK = 64;
+constexpr int kRowPad = kBK + 8;                    // bf16 per LDS row (16 B pad)
+constexpr int kStageElems = 2 * kBM * kRowPad;      // A and B of one stage
+constexpr size_t kLdsBytes = 2 * kStageElems * 2;   // two stages, bf16
+constexpr int kHalf = 128;                          // columns per partial
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.69314718055994531f;
+
+struct FusedArgs {
+    const uint16_t *h;     // [N, d]
+    const uint16_t *w;     // [V, d]
+    float2 *partial;       // [n_half, N]
+    int64_t n_rows;
+    int32_t vocab;
+    int32_t d;
+    int32_t n_half;
+    int32_t tiles_m, tiles_n, super_cols;
+};
+
+__device__ __forceinline__ float ex2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+__global__ __launch_bounds__(256, 1) void fused_lse_kernel(FusedArgs a) {
+    extern __shared__ __attribute__((aligned(16))) uint16_t lds[];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wm = wave >> 1, wn = wave & 1;
+
+    // ---- tile of this workgroup (XCD-aware order) ----
+    const int b = blockIdx.x;
+    const int xcd = b & 7, s = b >> 3;
+    const int S = s >> 5, q = s & 31;
+    const int tm = (S / a.super_cols) * 16 + (xcd >> 1) * 4 + (q & 3);
+    const int tn = (S % a.super_cols) * 16 + (xcd & 1) * 8 + (q >> 2);
+    if (tm >= a.tiles_m || tn >= a.tiles_n) return;
+    const int64_t m0 = (int64_t)tm * kBM;
+    const int64_t n0 = (int64_t)tn * kBN;
+    const int d = a.d;
+
+    // ---- global -> register staging: thread owns 8 A and 8 B 16-byte chunks ----
+    const int crow = tid >> 3, ckc = tid & 7;  // chunk row within a 32-row slab, k chunk
+    const u32x4 zero4 = {0u, 0u, 0u, 0u};
+    u32x4 ra[8], rb[8];
+    auto load_block = [&](int k0) {
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            const int64_t r = m0 + crow + 32 * i;
+            ra[i] = (r < a.n_rows)
+                        ? *reinterpret_cast<const u32x4 *>(a.h + r * d + k0 + ckc * 8)
+                        : zero4;
+            const int64_t c = n0 + crow + 32 * i;
+            rb[i] = (c < a.vocab)
+                        ? *reinterpret_cast<const u32x4 *>(a.w + c * d + k0 + ckc * 8)
+                        : zero4;
+        }
+    };
+    auto store_block = [&](int stage) {
+        uint16_t *As = lds + stage * kStageElems;
+        uint16_t *Bs = As + kBM * kRowPad;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            *reinterpret_cast<u32x4 *>(As + (crow + 32 * i) * kRowPad + ckc * 8) = ra[i];
+            *reinterpret_cast<u32x4 *>(Bs + (crow + 32 * i) * kRowPad + ckc * 8) = rb[i];
+        }
+    };
+
+    f32x16 acc[4][4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+#pragma unroll
+            for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.0f;
+
+    const int nk = d / kBK;
+    load_block(0);
+    store_block(0);
+    __syncthreads();
+    const int frag_row = lane & 31, frag_k = 8 * (lane >> 5);
+    for (int kb = 0; kb < nk; ++kb) {
+        if (kb + 1 < nk) load_block((kb + 1) * kBK);
+        const uint16_t *As = lds + (kb & 1) * kStageElems + (wm * 128) * kRowPad;
+        const uint16_t *Bs = lds + (kb & 1) * kStageElems + kBM * kRowPad + (wn * 128) * kRowPad;
+#pragma unroll
+        for (int kk = 0; kk < kBK; kk += 16) {
+            bf16x8 fa[4], fb[4];
+#pragma unroll
+            for (int t = 0; t < 4; ++t) {
+                fa[t] = *reinterpret_cast<const bf16x8 *>(As + (t * 32 + frag_row) * kRowPad + kk + frag_k);
+                fb[t] = *reinterpret_cast<const bf16x8 *>(Bs + (t * 32 + frag_row) * kRowPad + kk + frag_k);
+            }
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
+        }
+        if (kb + 1 < nk) store_block((kb + 1) & 1);
+        __syncthreads();
+    }
+
+    // ---- epilogue: per row of this wave's 128 columns, (max, sum exp(z - max)) ----
+    float2 *stage = reinterpret_cast<float2 *>(lds) + wave * 128;  // LDS is free after the loop
+    const int col_lane = lane & 31, half = lane >> 5;
+    bool col_ok[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) col_ok[j] = (n0 + wn * 128 + j * 32 + col_lane) < a.vocab;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            float v[4];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) v[j] = col_ok[j] ? acc[i][j][r] : -INFINITY;
+            float m = fmaxf(fmaxf(v[0], v[1]), fmaxf(v[2], v[3]));
+#pragma unroll
+            for (int off = 1; off < 32; off <<= 1) m = fmaxf(m, __shfl_xor(m, off, 64));
+            const float ref = (m == -INFINITY) ? 0.0f : m;
+            const float mref = ref * kLog2e;
+            float sum = 0.0f;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) sum += ex2(__builtin_fmaf(v[j], kLog2e, -mref));
+#pragma unroll
+            for (int off = 1; off < 32; off <<= 1) sum += __shfl_xor(sum, off, 64);
+            const int row_local = i * 32 + (r >> 2) * 8 + half * 4 + (r & 3);
+            if (col_lane == 0) stage[row_local] = make_float2(m, sum);
+        }
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+    const int hidx = tn * 2 + wn;
+    if (hidx < a.n_half) {
+#pragma unroll
+        for (int p = 0; p < 2; ++p) {
+            const int rl = p * 64 + lane;
+            const int64_t row = m0 + wm * 128 + rl;
+            if (row < a.n_rows) a.partial[(int64_t)hidx * a.n_rows + row] = stage[rl];
+        }
+    }
+}
+
+// z_y = h . w_y, one wave per row, fp32.
+__global__ __launch_bounds__(256) void fused_gather_kernel(const uint16_t *h, const uint16_t *w,
+                                                           const int32_t *ids, float *zy,
+                                                           int64_t n_rows, int32_t vocab, int32_t d) {
+    const int lane = threadIdx.x & 63;
+    const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (row >= n_rows) return;
+    const int32_t y = ids[row];
+    if (y < 0 || y >= vocab) {
+        if (lane == 0) zy[row] = __builtin_nanf("");
+        return;
+    }
+    const u32x4 *hp = reinterpret_cast<const u32x4 *>(h + row * d);
+    const u32x4 *wp = reinterpret_cast<const u32x4 *>(w + (int64_t)y * d);
+    float acc = 0.0f;
+    for (int c = lane; c < d / 8; c += 64) {
+        const u32x4 x = hp[c], z = wp[c];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            acc = __builtin_fmaf(__uint_as_float(x[e] << 16), __uint_as_float(z[e] << 16), acc);
+            acc = __builtin_fmaf(__uint_as_float(x[e] & 0xFFFF0000u), __uint_as_float(z[e] & 0xFFFF0000u), acc);
+        }
+    }
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) acc += __shfl_xor(acc, off, 64);
+    if (lane == 0) zy[row] = acc;
+}
+
+// Merge the V/128 partials of each row and finish log pi_T(y).
+__global__ __launch_bounds__(256) void fused_merge_kernel(const float2 *partial, const float *zy,
+                                                          const int32_t *ids, float *logp_t,
+                                                          int64_t n_rows, int32_t n_half,
+                                                          int32_t vocab, uint32_t *flags) {
+    const int64_t row = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (row >= n_rows) return;
+    float m = -INFINITY, s = 0.0f;
+    for (int j = 0; j < n_half; ++j) {
+        const float2 p = partial[(int64_t)j * n_rows + row];
+        const float mn = fmaxf(m, p.x);
+        const float ref = (mn == -INFINITY) ? 0.0f : mn;
+        s = s * ex2((m - ref) * kLog2e) + p.y * ex2((p.x - ref) * kLog2e);
+        m = mn;
+    }
+    const int32_t y = ids[row];
+    uint32_t bad = 0;
+    if (!((m > -INFINITY) && (m < INFINITY) && (s > 0.0f) && (s < INFINITY))) bad |= STRIDE_FLAG_NONFINITE;
+    if (y < 0 || y >= vocab) bad |= STRIDE_FLAG_TOKEN_OOB;
+    const float z = zy[row];
+    if (!bad && !(z > -INFINITY && z < INFINITY)) bad |= STRIDE_FLAG_NONFINITE;
+    if (bad) {
+        raise_flag(flags, bad);
+        logp_t[row] = __builtin_nanf("");
+    } else {
+        logp_t[row] = (z - m) - __builtin_amdgcn_logf(s) * kLn2;
+    }
+}
+
+}  // namespace
+
+size_t fused_ws_bytes(int64_t n_rows, int32_t vocab) {
+    const int64_t n_half = ((int64_t)vocab + kHalf - 1) / kHalf;
+    return (size_t)n_half * n_rows * sizeof(float2) + (size_t)n_rows * sizeof(float) + 256;
+}
+
+hipError_t launch_fused_teacher(const uint16_t *h, const uint16_t *w, const int32_t *ids,
+                                float *logp_t, int64_t n_rows, int32_t vocab, int32_t d,
+                                uint32_t *flags, void *ws, hipStream_t stream) {
+    if (n_rows == 0) return hipSuccess;
+    FusedArgs a;
+    a.h = h;
+    a.w = w;
+    a.n_rows = n_rows;
+    a.vocab = vocab;
+    a.d = d;
+    a.n_half = (vocab + kHalf - 1) / kHalf;
+    a.tiles_m = (int)((n_rows + kBM - 1) / kBM);
+    a.tiles_n = (vocab + kBN - 1) / kBN;
+    a.super_cols = (a.tiles_n + 15) / 16;
+    const int super_rows = (a.tiles_m + 15) / 16;
+    a.partial = static_cast<float2 *>(ws);
+    float *zy = reinterpret_cast<float *>(static_cast<char *>(ws) +
+                                          (size_t)a.n_half * n_rows * sizeof(float2));
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(fused_lse_kernel),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)kLdsBytes);
+    if (e != hipSuccess) return e;
+    const int64_t blocks = (int64_t)super_rows * a.super_cols * 256;
+    hipLaunchKernelGGL(fused_lse_kernel, dim3((unsigned)blocks), dim3(256), kLdsBytes, stream, a);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(fused_gather_kernel, dim3((unsigned)((n_rows + 3) / 4)), dim3(256), 0, stream,
+                       h, w, ids, zy, n_rows, vocab, d);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(fused_merge_kernel, dim3((unsigned)((n_rows + 255) / 256)), dim3(256), 0,
+                       stream, a.partial, zy, ids, logp_t, n_rows, a.n_half, vocab, flags);
+    return hipGetLastError();
+}
+
+}  // namespace stride

@@ -159,15 +159,57 @@ stride_status stride_score(const stride_layout *layout, int32_t vocab, int64_t l
     return ok();
 }
 
+size_t stride_fused_workspace_size(const stride_layout *layout, int32_t vocab) {
+    if (!layout || vocab < 1 || layout->n_tokens < 0) return 0;
+    return fused_ws_bytes(layout->n_tokens, vocab);
+}
+
 stride_status stride_score_fused(const stride_layout *layout, int32_t vocab, int32_t d,
                                  const void *hidden_t, const void *w_t, const void *student_logits,
                                  int64_t ld, const int32_t *token_ids, float *logp_t, float *logp_s,
                                  float *kl, double *turn_mean, uint32_t *dev_flags, void *ws,
                                  size_t ws_bytes, hipStream_t stream) {
-    (void)layout; (void)vocab; (void)d; (void)hidden_t; (void)w_t; (void)student_logits; (void)ld;
-    (void)token_ids; (void)logp_t; (void)logp_s; (void)kl; (void)turn_mean; (void)dev_flags;
-    (void)ws; (void)ws_bytes; (void)stream;
-    return fail(STRIDE_ERR_UNSUPPORTED, "stride_score_fused is not available in this build");
+    stride_status st = check_layout(layout);
+    if (st != STRIDE_OK) return st;
+    const stride_layout &L = *layout;
+    if (vocab < 1) return fail(STRIDE_ERR_INVALID_ARG, "vocab = %d < 1", vocab);
+    if (d < 64 || d % 64 != 0)
+        return fail(STRIDE_ERR_UNSUPPORTED, "hidden size d = %d is not a positive multiple of 64", d);
+    if (!student_logits && (logp_s || kl))
+        return fail(STRIDE_ERR_INVALID_ARG, "logp_s / kl requested without student logits");
+    if (L.n_tokens > 0) {
+        if (!hidden_t || !w_t) return fail(STRIDE_ERR_INVALID_ARG, "hidden_t or w_t is NULL");
+        if (!aligned(hidden_t, 16) || !aligned(w_t, 16))
+            return fail(STRIDE_ERR_UNSUPPORTED, "hidden_t and w_t must be 16-byte aligned");
+        if (!token_ids || !logp_t) return fail(STRIDE_ERR_INVALID_ARG, "token_ids or logp_t is NULL");
+        if (student_logits) {
+            if (ld < vocab)
+                return fail(STRIDE_ERR_INVALID_ARG, "ld = %lld < vocab = %d", (long long)ld, vocab);
+            if ((ld * 2) % 16 != 0 || !aligned(student_logits, 16))
+                return fail(STRIDE_ERR_UNSUPPORTED, "student rows must be 16-byte aligned");
+        }
+    }
+    if (L.n_turns > 0 && !turn_mean) return fail(STRIDE_ERR_INVALID_ARG, "turn_mean is NULL");
+    const size_t need = fused_ws_bytes(L.n_tokens, vocab);
+    if (!ws) return fail(STRIDE_ERR_WORKSPACE, "workspace is NULL (need %zu bytes)", need);
+    if (!aligned(ws, 256)) return fail(STRIDE_ERR_WORKSPACE, "workspace is not 256-byte aligned");
+    if (ws_bytes < need)
+        return fail(STRIDE_ERR_WORKSPACE, "workspace has %zu bytes, need %zu", ws_bytes, need);
+
+    hipError_t e = launch_fused_teacher(static_cast<const uint16_t *>(hidden_t),
+                                        static_cast<const uint16_t *>(w_t), token_ids, logp_t,
+                                        L.n_tokens, vocab, d, dev_flags, ws, stream);
+    if (e != hipSuccess) return hip_fail(e, "fused projection launch");
+    if (student_logits) {
+        PtrTable sp{};
+        sp.p[0] = student_logits;
+        e = launch_score_rows(STRIDE_BF16, sp, 1, nullptr, nullptr, token_ids, logp_s, nullptr,
+                              L.n_tokens, vocab, ld, dev_flags, stream);
+        if (e != hipSuccess) return hip_fail(e, "student scoring launch");
+    }
+    e = launch_turn_mean(L, logp_t, logp_s, kl, turn_mean, dev_flags, stream);
+    if (e != hipSuccess) return hip_fail(e, "turn-mean launch");
+    return ok();
 }
 
 stride_status stride_stop(const stride_layout *layout, int32_t unit, const void *values,

@@ -59,6 +59,8 @@ def _load():
     lib.stride_score_fused.argtypes = [lp, i32, i32, vp, vp, vp, i64, vp, vp, vp, vp, vp, vp, vp,
                                        sz, vp]
     lib.stride_score_fused.restype = i32
+    lib.stride_fused_workspace_size.argtypes = [lp, i32]
+    lib.stride_fused_workspace_size.restype = sz
     lib.stride_stop.argtypes = [lp, i32, vp, vp, i32, vp, vp, vp, vp, vp, vp, sz, vp]
     lib.stride_stop.restype = i32
     lib.stride_restart_turn.argtypes = [lp, i32, vp, vp, vp, i32, vp, vp, vp, vp, vp, vp]
@@ -136,6 +138,10 @@ def stride_workspace_size(layout: Layout, unit: int) -> int:
     return int(_lib.stride_workspace_size(layout.c(), unit))
 
 
+def stride_fused_workspace_size(layout: Layout, vocab: int) -> int:
+    return int(_lib.stride_fused_workspace_size(layout.c(), int(vocab)))
+
+
 def stride_score(layout: Layout, vocab: int, teacher_logits: Sequence[torch.Tensor],
                  student_logits: torch.Tensor | None, token_ids: torch.Tensor, logp_t: torch.Tensor,
                  logp_s: torch.Tensor | None, kl: torch.Tensor | None, turn_mean: torch.Tensor,
@@ -198,7 +204,7 @@ class Path:
     current stream with no host synchronisation; outputs stay on the device."""
 
     def __init__(self, layout: Layout, unit: int, with_student: bool = True,
-                 device: str | torch.device = "cuda"):
+                 device: str | torch.device = "cuda", fused_vocab: int | None = None):
         self.layout, self.unit = layout, unit
         n, t, r = layout.n_tokens, layout.n_turns, layout.n_rollouts
         f32 = dict(dtype=torch.float32, device=device)
@@ -216,6 +222,10 @@ class Path:
         self.flags = torch.zeros(1, dtype=torch.int32, device=device)
         ws_bytes = max(stride_workspace_size(layout, unit), 256)
         self.ws = torch.empty(ws_bytes, dtype=torch.uint8, device=device)
+        self.fused_ws = None
+        if fused_vocab is not None:
+            self.fused_ws = torch.empty(max(stride_fused_workspace_size(layout, fused_vocab), 256),
+                                        dtype=torch.uint8, device=device)
 
     def values(self) -> torch.Tensor:
         return self.turn_mean if self.unit == STRIDE_UNIT_TURN else self.logp_t
@@ -223,6 +233,10 @@ class Path:
     def score(self, vocab, teachers, student, token_ids, stream=None):
         stride_score(self.layout, vocab, teachers, student, token_ids, self.logp_t, self.logp_s,
                      self.kl, self.turn_mean, self.flags, self.ws, stream)
+
+    def score_fused(self, vocab, hidden, w, student, token_ids, stream=None):
+        stride_score_fused(self.layout, vocab, hidden, w, student, token_ids, self.logp_t,
+                           self.logp_s, self.kl, self.turn_mean, self.flags, self.fused_ws, stream)
 
     def stop(self, lam, start_unit=None, stream=None):
         stride_stop(self.layout, self.unit, self.values(), lam, start_unit, self.cum,

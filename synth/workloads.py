@@ -22,9 +22,10 @@ and AIME scored by Qwen3 models, none of which exist here):
   multi       32 rollouts x 8 turns x 512 tokens, two teachers, domain
               ~ Bernoulli(1/2); teacher boosts ~N(5, 2) and ~N(3, 2); planted
               turn and mask as in agentic; one student shared by both.
-  fused       16 rollouts x 8 turns x 512 tokens; teacher logits h W with
-              h ~ N(0, 1) [N, 2048] and W ~ N(0, 0.02) [2048, V] (bf16); student
-              as in agentic; no planted turn.
+  fused       16 rollouts x 8 turns x 512 tokens; teacher logits z = h W with
+              h ~ N(0, 1) [N, 2048] and W ~ N(0, 0.02) [2048, V] (bf16), W held as
+              a linear layer stores it ([V, 2048], row v = entry v); student as
+              in agentic; no planted turn.
 
 N(mu, s) means mean mu and standard deviation s.  Elements are Irwin-Hall(12)
 approximations of a normal draw (``synth.hip``).
@@ -193,9 +194,10 @@ class Workload:
         return out
 
     def w_host(self, threads: int = 8) -> np.ndarray:
+        """lm_head weight as a linear layer stores it: [V, d], row v = vocabulary entry v."""
         d, v = self.fused_d, self.vocab
-        out = np.zeros((d, v), np.uint16)
-        self._fill_host(out, v, v, BF16, 0, d, STREAM_W, self.w_sigma, None, None, threads)
+        out = np.zeros((v, d), np.uint16)
+        self._fill_host(out, d, d, BF16, 0, v, STREAM_W, self.w_sigma, None, None, threads)
         return out
 
     # ---------------------------------------------------------- device fills

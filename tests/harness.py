@@ -63,6 +63,60 @@ def device_inputs(wl: W.Workload, with_student: bool = True, device: str = "cuda
                 start=start)
 
 
+def device_inputs_fused(wl: W.Workload, device: str = "cuda"):
+    """Hidden states [N, d], lm_head weight [V, d] and student logits on the device."""
+    import torch
+    import paper_2609_14636_amd as P
+
+    stream = torch.cuda.current_stream().cuda_stream
+    rto = torch.from_numpy(wl.rollout_turn_off).to(device)
+    tto = torch.from_numpy(wl.turn_tok_off).to(device)
+    layout = P.Layout(rto, tto, wl.n_tokens, None)
+    ids = torch.from_numpy(wl.tok).to(device)
+    N, d, V = wl.n_tokens, wl.fused_d, wl.vocab
+    hidden = torch.empty((N, d), dtype=torch.bfloat16, device=device)
+    w = torch.empty((V, d), dtype=torch.bfloat16, device=device)
+    if N:
+        wl.fill_device(hidden.data_ptr(), d, d, W.BF16, 0, N, W.STREAM_HIDDEN, wl.hidden_sigma,
+                       None, None, stream)
+    wl.fill_device(w.data_ptr(), d, d, W.BF16, 0, V, W.STREAM_W, wl.w_sigma, None, None, stream)
+    sboost = torch.from_numpy(wl.student_boost).to(device)
+    student = torch.empty((N, wl.ld), dtype=torch.bfloat16, device=device)
+    if N:
+        wl.fill_device(student.data_ptr(), V, wl.ld, W.BF16, 0, N, W.STREAM_STUDENT,
+                       wl.student_sigma, ids.data_ptr(), sboost.data_ptr(), stream)
+    return dict(layout=layout, ids=ids, hidden=hidden, w=w, student=student, mask=None, start=None)
+
+
+def run_gpu_fused(wl: W.Workload, lam, alpha, inp=None):
+    import torch
+    import paper_2609_14636_amd as P
+
+    inp = inp or device_inputs_fused(wl)
+    path = P.Path(inp["layout"], wl.unit, with_student=True, fused_vocab=wl.vocab)
+    path.score_fused(wl.vocab, inp["hidden"], inp["w"], inp["student"], inp["ids"])
+    path.stop(lam, inp["start"])
+    path.restart(alpha, inp["mask"])
+    torch.cuda.synchronize()
+    return path.host()
+
+
+def oracle_fused_scores(wl: W.Workload, rows, w_dv=None, threads: int = 16):
+    """Oracle teacher/student log-probabilities of the given rows of a fused workload.
+    The oracle takes the lm_head as the [d, V] matrix of z = h W, the transpose of the
+    [V, d] storage the GPU reads; both come from the host generator."""
+    if w_dv is None:
+        w_dv = np.ascontiguousarray(wl.w_host(threads).T)
+    rows = np.asarray(rows, np.int64)
+    h = np.concatenate([wl.hidden_host(int(r), 1, 1) for r in rows]) if rows.size else \
+        np.zeros((0, wl.fused_d), np.uint16)
+    ids = wl.tok[rows]
+    lt, _, ft = OP.O.fused_logp(h, w_dv, ids)
+    s = np.concatenate([wl.student_rows_host(int(r), 1, 1) for r in rows])
+    ls, _, fs = OP.O.logp_rows(s, ids, wl.vocab)
+    return {"logp_t": lt, "logp_s": ls, "kl": OP.O.token_kl(ls, lt), "flags": ft | fs}, w_dv
+
+
 def run_gpu(wl: W.Workload, lam, alpha, inp=None, with_student=True):
     import torch
     import paper_2609_14636_amd as P

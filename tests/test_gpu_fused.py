@@ -1,0 +1,93 @@
+"""Fused projection + log-sum-exp path (stride_score_fused) against the float64 oracle.
+
+The oracle forms z = h W in binary64 from the host-generated bf16 operands (it takes
+W as [d, V]; the GPU reads the same values stored as a linear layer's [V, d] weight)
+and never sees a GPU value.  Small shapes are compared on every row, including
+partial row and vocabulary tiles; the full-size workload on sampled rows and on one
+complete turn.
+"""
+import math
+import sys
+
+import numpy as np
+import pytest
+
+from synth import workloads as W
+from tests import harness as H
+from tests import workload_params as WP
+
+pytestmark = pytest.mark.gpu
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(autouse=True)
+def _gpu():
+    import torch
+    assert torch.cuda.is_available()
+    yield
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+
+
+def _per_rollout(wl, sc):
+    out = {}
+    for r in range(wl.n_rollouts):
+        a, b = wl.rollout_rows(r)
+        out[r] = {k: sc[k][a:b] for k in ("logp_t", "logp_s", "kl")}
+    return out
+
+
+@pytest.mark.parametrize("R,turns,tok,vocab,d", [
+    (2, 2, 64, 1000, 128),      # vocabulary tile partly filled, one row tile
+    (1, 3, 100, 4097, 192),     # 300 rows: a partial row tile; V not a multiple of 128
+    (2, 2, 150, 257, 64),       # one K block; last 128-column partial has one column
+    (2, 2, 24, 151936, 2048),   # the full hidden size and vocabulary on 96 rows
+])
+def test_fused_parity(R, turns, tok, vocab, d):
+    wl = W.make("fused", seed=3 + vocab, scale=dict(R=R, turns=turns, tok=tok, vocab=vocab, d=d))
+    say(f"[fused] N={wl.n_tokens} V={vocab} d={d}")
+    sc, _ = H.oracle_fused_scores(wl, np.arange(wl.n_tokens))
+    assert sc["flags"] == 0
+    per = _per_rollout(wl, sc)
+    tm, _ = H.OP.O.turn_mean(wl.turn_tok_off, sc["logp_t"])
+    c = WP.pooled_cum(wl.unit_off(), tm)
+    lam, alpha = [WP.midpoint_quantile(c, 0.5)], [-math.inf]
+    ora = {r: (per[r], H.oracle_rollout(wl, r, per[r], lam, alpha)) for r in per}
+    gpu = H.run_gpu_fused(wl, lam, alpha)
+    assert gpu["flags"] == 0, hex(gpu["flags"])
+    rep = H.compare(wl, gpu, ora, lam, alpha)
+    H.assert_invariants(gpu, wl)
+    say(f"[fused] {rep}")
+
+
+def test_fused_full_size():
+    """The fused workload at full size (65,536 rows, d = 2048, V = 151,936)."""
+    wl = W.make("fused", 1001)
+    lam, alpha = WP.fused_thresholds(wl.vocab, wl.fused_d, wl.hidden_sigma, wl.w_sigma)
+    gpu = H.run_gpu_fused(wl, lam, alpha)
+    assert gpu["flags"] == 0, hex(gpu["flags"])
+    H.assert_invariants(gpu, wl)
+    # one complete turn (rows of turn 5 of rollout 3) plus scattered rows, element by element
+    t = int(wl.rollout_turn_off[3]) + 5
+    a, b = int(wl.turn_tok_off[t]), int(wl.turn_tok_off[t + 1])
+    extra = np.array([0, 1, 255, 256, 4095, 32768, wl.n_tokens - 1])
+    rows = np.concatenate([np.arange(a, b), extra])
+    sc, _ = H.oracle_fused_scores(wl, rows)
+    for k in ("logp_t", "logp_s"):
+        d = np.max(np.abs(gpu[k][rows] - sc[k]))
+        assert d <= H.TOL_LOGP, (k, d)
+        say(f"[fused full] max |d {k}| over {rows.size} rows = {d:.2e}")
+    d = np.max(np.abs(gpu["kl"][rows] - sc["kl"]))
+    assert d <= H.TOL_KL, d
+    turn = math.fsum(sc["logp_t"][:b - a]) / (b - a)
+    assert abs(gpu["turn_mean"][t] - turn) <= H.TOL_LOGP, (gpu["turn_mean"][t], turn)
+    # every turn mean sits near the closed form -(log V + d s_h^2 s_W^2 / 2), so with
+    # lambda = 5.5 x that value every rollout stops on its sixth turn (index 5)
+    expect = lam[0] / 5.5
+    assert np.all(np.abs(gpu["turn_mean"] - expect) < 0.5), (gpu["turn_mean"].min(), expect)
+    assert gpu["stop_unit"].tolist() == [5] * wl.n_rollouts, gpu["stop_unit"]
+    assert gpu["k_max"].tolist() == [6] * wl.n_rollouts
