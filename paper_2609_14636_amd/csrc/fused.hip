@@ -9,10 +9,13 @@
 // Kernel 1 (MFMA): a 256 x 256 tile of z per workgroup, K = d streamed in
 //   64-wide blocks through double-buffered LDS (rows padded by 16 B), four
 //   waves in a 2 x 2 grid each holding a 128 x 128 fp32 accumulator (16
-//   v_mfma_f32_32x32x16_bf16 tiles).  Both operands are K-contiguous, so each
-//   MFMA operand is one 16-byte LDS read.  The epilogue reduces every row of
-//   each wave's 128 columns to (max, sum of exp(z - max)) with a 32-lane
-//   butterfly and writes it to a partial table [V/128][N] (rows contiguous).
+//   v_mfma_f32_32x32x16_bf16 tiles); the fragments of the next 16-wide k step
+//   are read while the current one multiplies.  Both operands are
+//   K-contiguous, so each MFMA operand is one 16-byte LDS read.  W is the A
+//   operand and H the B operand, so each lane's accumulators hold 64 of one
+//   token's 128 logits and its partner lane (l ^ 32) the other 64: the
+//   epilogue reduces a token to (max, sum of exp(z - max)) with one exchange
+//   and writes it to a partial table [V/128][N] (tokens contiguous).
 //   Workgroups are numbered so that the 32 resident on one XCD (dispatch is
 //   round-robin over the 8 XCDs) cover a 4 x 8 block of tiles of a 16 x 16
 //   super-tile, and super-tiles advance along V: each XCD's L2 serves every
@@ -94,6 +97,9 @@ __global__ __launch_bounds__(256, 1) void fused_lse_kernel(FusedArgs a) {
         }
     };
 
+    // acc[i][j]: vocabulary 32-block i of this wave's 128 entries x token 32-block j of its
+    // 128 tokens.  With W as the MFMA A operand and H as B, lane l holds token j*32 + l%32
+    // and 16 vocabulary entries of it, so a row's reduction stays inside a lane pair.
     f32x16 acc[4][4];
 #pragma unroll
     for (int i = 0; i < 4; ++i)
@@ -107,66 +113,77 @@ __global__ __launch_bounds__(256, 1) void fused_lse_kernel(FusedArgs a) {
     store_block(0);
     __syncthreads();
     const int frag_row = lane & 31, frag_k = 8 * (lane >> 5);
+    // wave (wv, wt): vocabulary half wv, token half wt of the 256 x 256 tile
+    const int wv = wn, wt = wm;
     for (int kb = 0; kb < nk; ++kb) {
         if (kb + 1 < nk) load_block((kb + 1) * kBK);
-        const uint16_t *As = lds + (kb & 1) * kStageElems + (wm * 128) * kRowPad;
-        const uint16_t *Bs = lds + (kb & 1) * kStageElems + kBM * kRowPad + (wn * 128) * kRowPad;
+        const uint16_t *Hs = lds + (kb & 1) * kStageElems + (wt * 128) * kRowPad;
+        const uint16_t *Ws = lds + (kb & 1) * kStageElems + kBM * kRowPad + (wv * 128) * kRowPad;
+        bf16x8 fw[2][4], fh[2][4];
 #pragma unroll
-        for (int kk = 0; kk < kBK; kk += 16) {
-            bf16x8 fa[4], fb[4];
+        for (int t = 0; t < 4; ++t) {
+            fw[0][t] = *reinterpret_cast<const bf16x8 *>(Ws + (t * 32 + frag_row) * kRowPad + frag_k);
+            fh[0][t] = *reinterpret_cast<const bf16x8 *>(Hs + (t * 32 + frag_row) * kRowPad + frag_k);
+        }
 #pragma unroll
-            for (int t = 0; t < 4; ++t) {
-                fa[t] = *reinterpret_cast<const bf16x8 *>(As + (t * 32 + frag_row) * kRowPad + kk + frag_k);
-                fb[t] = *reinterpret_cast<const bf16x8 *>(Bs + (t * 32 + frag_row) * kRowPad + kk + frag_k);
+        for (int kq = 0; kq < kBK / 16; ++kq) {
+            const int cur = kq & 1;
+            if (kq + 1 < kBK / 16) {
+#pragma unroll
+                for (int t = 0; t < 4; ++t) {
+                    fw[cur ^ 1][t] = *reinterpret_cast<const bf16x8 *>(
+                        Ws + (t * 32 + frag_row) * kRowPad + (kq + 1) * 16 + frag_k);
+                    fh[cur ^ 1][t] = *reinterpret_cast<const bf16x8 *>(
+                        Hs + (t * 32 + frag_row) * kRowPad + (kq + 1) * 16 + frag_k);
+                }
             }
 #pragma unroll
             for (int i = 0; i < 4; ++i)
 #pragma unroll
                 for (int j = 0; j < 4; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fw[cur][i], fh[cur][j],
+                                                                        acc[i][j], 0, 0, 0);
         }
         if (kb + 1 < nk) store_block((kb + 1) & 1);
         __syncthreads();
     }
 
-    // ---- epilogue: per row of this wave's 128 columns, (max, sum exp(z - max)) ----
-    float2 *stage = reinterpret_cast<float2 *>(lds) + wave * 128;  // LDS is free after the loop
-    const int col_lane = lane & 31, half = lane >> 5;
-    bool col_ok[4];
+    // ---- epilogue: per token of this wave, (max, sum exp(z - max)) over its 128 entries ----
+    const int half = lane >> 5;
+    const int64_t v_base = n0 + wv * 128;
+    const int vlim = (int)((a.vocab - v_base) < 128 ? (a.vocab - v_base) : 128);  // valid entries
+    const int hidx = tn * 2 + wv;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) col_ok[j] = (n0 + wn * 128 + j * 32 + col_lane) < a.vocab;
+    for (int j = 0; j < 4; ++j) {
+        float vals[64];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
+        for (int i = 0; i < 4; ++i)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-            float v[4];
+            for (int r = 0; r < 16; ++r) vals[i * 16 + r] = acc[i][j][r];
+        if (vlim < 128) {
 #pragma unroll
-            for (int j = 0; j < 4; ++j) v[j] = col_ok[j] ? acc[i][j][r] : -INFINITY;
-            float m = fmaxf(fmaxf(v[0], v[1]), fmaxf(v[2], v[3]));
+            for (int i = 0; i < 4; ++i)
 #pragma unroll
-            for (int off = 1; off < 32; off <<= 1) m = fmaxf(m, __shfl_xor(m, off, 64));
-            const float ref = (m == -INFINITY) ? 0.0f : m;
-            const float mref = ref * kLog2e;
-            float sum = 0.0f;
-#pragma unroll
-            for (int j = 0; j < 4; ++j) sum += ex2(__builtin_fmaf(v[j], kLog2e, -mref));
-#pragma unroll
-            for (int off = 1; off < 32; off <<= 1) sum += __shfl_xor(sum, off, 64);
-            const int row_local = i * 32 + (r >> 2) * 8 + half * 4 + (r & 3);
-            if (col_lane == 0) stage[row_local] = make_float2(m, sum);
+                for (int r = 0; r < 16; ++r)
+                    if (i * 32 + (r >> 2) * 8 + half * 4 + (r & 3) >= vlim) vals[i * 16 + r] = -INFINITY;
         }
-    }
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
-    const int hidx = tn * 2 + wn;
-    if (hidx < a.n_half) {
+        float m = vals[0];
 #pragma unroll
-        for (int p = 0; p < 2; ++p) {
-            const int rl = p * 64 + lane;
-            const int64_t row = m0 + wm * 128 + rl;
-            if (row < a.n_rows) a.partial[(int64_t)hidx * a.n_rows + row] = stage[rl];
+        for (int e = 1; e < 64; ++e) m = fmaxf(m, vals[e]);
+        m = fmaxf(m, __shfl_xor(m, 32, 64));
+        const float ref = (m == -INFINITY) ? 0.0f : m;
+        const float mref = ref * kLog2e;
+        float s0 = 0.0f, s1 = 0.0f;
+#pragma unroll
+        for (int e = 0; e < 64; e += 2) {
+            s0 += ex2(__builtin_fmaf(vals[e], kLog2e, -mref));
+            s1 += ex2(__builtin_fmaf(vals[e + 1], kLog2e, -mref));
         }
+        float sum = s0 + s1;
+        sum += __shfl_xor(sum, 32, 64);
+        const int64_t row = m0 + wt * 128 + j * 32 + (lane & 31);
+        if (half == 0 && hidx < a.n_half && row < a.n_rows)
+            a.partial[(int64_t)hidx * a.n_rows + row] = make_float2(m, sum);
     }
 }
 
