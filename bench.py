@@ -207,6 +207,8 @@ def main():
                     help="bound on the oracle sample: whole rollouts are added until the oracle "
                          "has computed this long (at least one rollout)")
     ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--exact-kl", action="store_true",
+                    help="also compute the exact full-vocabulary KL per token (paired kernel)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="only run a plain elementwise copy (torch.neg on float32) reading and "
                          "writing BYTES each per dispatch, to calibrate the HBM byte counters; keep "
@@ -244,7 +246,7 @@ def main():
     log(f"[bench] workload {args.workload} seed {args.seed}: R={wl.n_rollouts} T={wl.n_turns} "
         f"N={wl.n_tokens} V={wl.vocab}; generating {2 * wl.logits_bytes() / 1e9:.1f} GB on device")
     inp = H.device_inputs(wl)
-    path = P.Path(inp["layout"], wl.unit, with_student=True)
+    path = P.Path(inp["layout"], wl.unit, with_student=True, exact_kl=args.exact_kl)
     stream = torch.cuda.current_stream()
     torch.cuda.synchronize()
 
@@ -283,7 +285,7 @@ def main():
     per_token = 2 * wl.vocab * wl.esize + 4 + 8  # two logit rows in, token id in, two logps out
     bytes_alg = per_token * n_tok
     achieved = bytes_alg / (score_ms * 1e-3) / 1e9
-    traffic = measured_traffic(args.workload)
+    traffic = None if args.exact_kl else measured_traffic(args.workload)
     res = {
         "metric": METRIC,
         "value": n_tok / (ms_step * 1e-3),
@@ -303,7 +305,8 @@ def main():
                    "parallelism": "single GPU"},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
-                     "kernel": "score_rows_kernel<bf16>", "kernel_ms": score_ms,
+                     "kernel": ("score_pairs_kernel<bf16> (with exact KL)" if args.exact_kl
+                                else "score_rows_kernel<bf16>"), "kernel_ms": score_ms,
                      "bytes_per_launch": bytes_alg},
     }
     if not args.no_cpu:

@@ -106,14 +106,19 @@ size_t stride_workspace_size(const stride_layout *layout, int32_t unit);
  *   token_ids        [N] int32, the sampled tokens
  *   logp_t, logp_s   [N] float outputs (logp_s may be NULL)
  *   kl               [N] float output log pi_S - log pi_T, or NULL
+ *   kl_full          [N] float output or NULL: the exact reverse KL over the whole
+ *                    vocabulary, KL(pi_S || pi_T) = sum_v pi_S(v) log(pi_S(v) / pi_T(v)),
+ *                    the divergence whose sequence-level form OPD minimises (Sec. 3.1);
+ *                    needs student_logits.  Computed in the same single pass over both
+ *                    rows (one wavefront reads the token's teacher and student rows).
  *   turn_mean        [T] double output
  *   dev_flags        device uint32 or NULL
  */
 stride_status stride_score(const stride_layout *layout, int32_t vocab, int64_t ld, int32_t dtype,
                            int32_t n_teachers, const void *const *teacher_logits,
                            const void *student_logits, const int32_t *token_ids, float *logp_t,
-                           float *logp_s, float *kl, double *turn_mean, uint32_t *dev_flags,
-                           void *ws, size_t ws_bytes, hipStream_t stream);
+                           float *logp_s, float *kl, float *kl_full, double *turn_mean,
+                           uint32_t *dev_flags, void *ws, size_t ws_bytes, hipStream_t stream);
 
 /*
  * As stride_score, with the teacher's logits produced by its output

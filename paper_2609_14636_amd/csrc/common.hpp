@@ -56,6 +56,11 @@ hipError_t launch_score_rows(int32_t dtype, const PtrTable &teachers, int32_t n_
                              float *logp_t, float *logp_s, int64_t n_rows, int32_t vocab,
                              int64_t ld, uint32_t *flags, hipStream_t stream);
 
+hipError_t launch_score_pairs(int32_t dtype, const PtrTable &teachers, int32_t n_teachers,
+                              const uint8_t *row_dom, const void *student, const int32_t *ids,
+                              float *logp_t, float *logp_s, float *kl_full, int64_t n_rows,
+                              int32_t vocab, int64_t ld, uint32_t *flags, hipStream_t stream);
+
 // turn.hip
 hipError_t launch_turn_mean(const stride_layout &L, const float *logp_t, const float *logp_s,
                             float *kl, double *turn_mean, uint32_t *flags, hipStream_t stream);

@@ -188,6 +188,160 @@ __global__ __launch_bounds__(256) void score_rows_kernel(ScoreArgs a) {
     }
 }
 
+// Exact reverse KL in the same pass: one wavefront per token streams the teacher
+// and the student row together.  With p_S(v) = exp(s_v - LSE_S),
+//   KL(pi_S || pi_T) = sum_v p_S(v) (s_v - t_v) - LSE_S + LSE_T
+//                    = A / Z_S - LSE_S + LSE_T,  A = sum_v exp(s_v - m_S) (s_v - t_v),
+// and A rescales with the student's running maximum exactly like Z_S.
+template <int N>
+__device__ __forceinline__ void fold_pair(float &mt, float &zt, float &ms, float &zs, float &am,
+                                          const float *t, const float *x) {
+    float ct = t[0], cs = x[0];
+#pragma unroll
+    for (int i = 1; i < N; ++i) {
+        ct = fmaxf(ct, t[i]);
+        cs = fmaxf(cs, x[i]);
+    }
+    const float mtn = fmaxf(mt, ct), msn = fmaxf(ms, cs);
+    const float rt = (mtn == -INFINITY) ? 0.0f : mtn;
+    const float rs = (msn == -INFINITY) ? 0.0f : msn;
+    zt *= fast_exp2((mt - rt) * kLog2e);
+    const float ss = fast_exp2((ms - rs) * kLog2e);
+    zs *= ss;
+    am *= ss;
+    const float rtl = rt * kLog2e, rsl = rs * kLog2e;
+#pragma unroll
+    for (int i = 0; i < N; ++i) {
+        zt += fast_exp2(__builtin_fmaf(t[i], kLog2e, -rtl));
+        const float e = fast_exp2(__builtin_fmaf(x[i], kLog2e, -rsl));
+        zs += e;
+        // an entry with no student mass adds nothing, even where t - s is infinite
+        if (e > 0.0f) am = __builtin_fmaf(e, x[i] - t[i], am);
+    }
+    mt = mtn;
+    ms = msn;
+}
+
+struct PairArgs {
+    PtrTable teachers;
+    const void *student;
+    const uint8_t *row_dom;
+    const int32_t *ids;
+    float *logp_t;
+    float *logp_s;
+    float *kl_full;
+    uint32_t *flags;
+    int64_t n_rows;
+    int64_t ld;
+    int32_t vocab;
+    int32_t n_teachers;
+};
+
+template <int DT, int U>
+__global__ __launch_bounds__(256) void score_pairs_kernel(PairArgs a) {
+    constexpr int E = Elem<DT>::kPerVec;
+    const int lane = threadIdx.x & (kWave - 1);
+    const int64_t row = (int64_t)blockIdx.x * (blockDim.x / kWave) + (threadIdx.x / kWave);
+    if (row >= a.n_rows) return;
+    const int d = a.row_dom ? (int)a.row_dom[row] : 0;
+    if (d >= a.n_teachers) {
+        if (lane == 0) {
+            a.logp_t[row] = __builtin_nanf("");
+            a.kl_full[row] = __builtin_nanf("");
+            a.logp_s[row] = __builtin_nanf("");
+        }
+        return;
+    }
+    const size_t off = (size_t)row * a.ld * Elem<DT>::kSize;
+    const u32x4 *pt = reinterpret_cast<const u32x4 *>(static_cast<const char *>(a.teachers.p[d]) + off);
+    const u32x4 *ps = reinterpret_cast<const u32x4 *>(static_cast<const char *>(a.student) + off);
+    const int64_t nvec = a.vocab / E;
+    const int tail = a.vocab % E;
+    float mt = -INFINITY, zt = 0.0f, ms = -INFINITY, zs = 0.0f, am = 0.0f;
+    int64_t k = 0;
+    constexpr int64_t kStep = (int64_t)U * kWave;
+    for (; k + kStep <= nvec; k += kStep) {
+        u32x4 vt[U], vs[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            vt[u] = __builtin_nontemporal_load(pt + k + u * kWave + lane);
+            vs[u] = __builtin_nontemporal_load(ps + k + u * kWave + lane);
+        }
+        float xt[U * E], xs[U * E];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            unpack<DT>(vt[u], xt + u * E);
+            unpack<DT>(vs[u], xs + u * E);
+        }
+        fold_pair<U * E>(mt, zt, ms, zs, am, xt, xs);
+    }
+    for (; k < nvec; k += kWave) {
+        if (k + lane < nvec) {
+            float xt[E], xs[E];
+            unpack<DT>(__builtin_nontemporal_load(pt + k + lane), xt);
+            unpack<DT>(__builtin_nontemporal_load(ps + k + lane), xs);
+            fold_pair<E>(mt, zt, ms, zs, am, xt, xs);
+        }
+    }
+    if (tail && lane == 0) {
+        float xt[E], xs[E];
+        unpack<DT>(pt[nvec], xt);
+        unpack<DT>(ps[nvec], xs);
+#pragma unroll
+        for (int j = 0; j < E; ++j)
+            if (j >= tail) {
+                xt[j] = -INFINITY;
+                xs[j] = -INFINITY;
+            }
+        fold_pair<E>(mt, zt, ms, zs, am, xt, xs);
+    }
+#pragma unroll
+    for (int o = kWave / 2; o > 0; o >>= 1) {
+        const float mt2 = __shfl_xor(mt, o, kWave), zt2 = __shfl_xor(zt, o, kWave);
+        const float ms2 = __shfl_xor(ms, o, kWave), zs2 = __shfl_xor(zs, o, kWave);
+        const float am2 = __shfl_xor(am, o, kWave);
+        merge(mt, zt, mt2, zt2);
+        const float mn = fmaxf(ms, ms2);
+        const float ref = (mn == -INFINITY) ? 0.0f : mn;
+        const float f1 = fast_exp2((ms - ref) * kLog2e), f2 = fast_exp2((ms2 - ref) * kLog2e);
+        zs = zs * f1 + zs2 * f2;
+        am = am * f1 + am2 * f2;
+        ms = mn;
+    }
+    if (lane == 0) {
+        const int32_t y = a.ids[row];
+        uint32_t bad = 0;
+        const bool fin_t = (mt > -INFINITY) && (mt < INFINITY) && (zt > 0.0f) && (zt < INFINITY);
+        const bool fin_s = (ms > -INFINITY) && (ms < INFINITY) && (zs > 0.0f) && (zs < INFINITY);
+        if (!fin_t || !fin_s) bad |= STRIDE_FLAG_NONFINITE;
+        const float lt = __builtin_amdgcn_logf(zt) * kLn2, ls = __builtin_amdgcn_logf(zs) * kLn2;
+        // sum_v p_S (log p_S - log p_T) = A/Z_S - (m_S + log Z_S) + (m_T + log Z_T)
+        // +inf when the teacher gives no mass where the student has some
+        float kl = bad ? __builtin_nanf("") : (am / zs - (ms - mt)) - (ls - lt);
+        if (!(kl == kl)) bad |= STRIDE_FLAG_NONFINITE;
+        a.kl_full[row] = kl;
+        if (y < 0 || y >= a.vocab) bad |= STRIDE_FLAG_TOKEN_OOB;
+        float rt, rs;
+        if (bad & (STRIDE_FLAG_TOKEN_OOB | (fin_t && fin_s ? 0u : STRIDE_FLAG_NONFINITE))) {
+            rt = rs = __builtin_nanf("");
+        } else {
+            float xt, xs;
+            if (DT == STRIDE_BF16) {
+                xt = __uint_as_float((uint32_t)(reinterpret_cast<const uint16_t *>(pt)[y]) << 16);
+                xs = __uint_as_float((uint32_t)(reinterpret_cast<const uint16_t *>(ps)[y]) << 16);
+            } else {
+                xt = reinterpret_cast<const float *>(pt)[y];
+                xs = reinterpret_cast<const float *>(ps)[y];
+            }
+            rt = (xt - mt) - lt;
+            rs = (xs - ms) - ls;
+        }
+        if (bad) raise_flag(a.flags, bad);
+        a.logp_t[row] = rt;
+        a.logp_s[row] = rs;
+    }
+}
+
 // Teacher index of every row: row -> turn (by offsets) -> rollout -> domain.
 // Rows outside every turn, or whose rollout's domain is out of range, get
 // kBadDomain and raise a flag, so the scoring kernel writes NaN for them.
@@ -237,6 +391,34 @@ __global__ __launch_bounds__(256) void row_domain_kernel(stride_layout L, int32_
 }
 
 }  // namespace
+
+hipError_t launch_score_pairs(int32_t dtype, const PtrTable &teachers, int32_t n_teachers,
+                              const uint8_t *row_dom, const void *student, const int32_t *ids,
+                              float *logp_t, float *logp_s, float *kl_full, int64_t n_rows,
+                              int32_t vocab, int64_t ld, uint32_t *flags, hipStream_t stream) {
+    if (n_rows == 0) return hipSuccess;
+    PairArgs a;
+    a.teachers = teachers;
+    a.student = student;
+    a.row_dom = row_dom;
+    a.ids = ids;
+    a.logp_t = logp_t;
+    a.logp_s = logp_s;
+    a.kl_full = kl_full;
+    a.flags = flags;
+    a.n_rows = n_rows;
+    a.ld = ld;
+    a.vocab = vocab;
+    a.n_teachers = n_teachers;
+    const int64_t blocks = (n_rows + 3) / 4;
+    if (dtype == STRIDE_BF16)
+        hipLaunchKernelGGL((score_pairs_kernel<STRIDE_BF16, 4>), dim3((unsigned)blocks), dim3(256), 0,
+                           stream, a);
+    else
+        hipLaunchKernelGGL((score_pairs_kernel<STRIDE_F32, 4>), dim3((unsigned)blocks), dim3(256), 0,
+                           stream, a);
+    return hipGetLastError();
+}
 
 hipError_t launch_row_domain(const stride_layout &L, int32_t n_teachers, uint8_t *row_dom,
                              uint32_t *flags, hipStream_t stream) {

@@ -103,8 +103,8 @@ const char *stride_last_error(void) { return g_err; }
 stride_status stride_score(const stride_layout *layout, int32_t vocab, int64_t ld, int32_t dtype,
                            int32_t n_teachers, const void *const *teacher_logits,
                            const void *student_logits, const int32_t *token_ids, float *logp_t,
-                           float *logp_s, float *kl, double *turn_mean, uint32_t *dev_flags,
-                           void *ws, size_t ws_bytes, hipStream_t stream) {
+                           float *logp_s, float *kl, float *kl_full, double *turn_mean,
+                           uint32_t *dev_flags, void *ws, size_t ws_bytes, hipStream_t stream) {
     stride_status st = check_layout(layout);
     if (st != STRIDE_OK) return st;
     const stride_layout &L = *layout;
@@ -119,8 +119,10 @@ stride_status stride_score(const stride_layout *layout, int32_t vocab, int64_t l
     if (n_teachers < 1 || n_teachers > STRIDE_MAX_DOMAINS)
         return fail(STRIDE_ERR_UNSUPPORTED, "n_teachers = %d outside 1..%d", n_teachers,
                     STRIDE_MAX_DOMAINS);
-    if (!student_logits && (logp_s || kl))
-        return fail(STRIDE_ERR_INVALID_ARG, "logp_s / kl requested without student logits");
+    if (!student_logits && (logp_s || kl || kl_full))
+        return fail(STRIDE_ERR_INVALID_ARG, "logp_s / kl / kl_full requested without student logits");
+    if (kl_full && !logp_s && L.n_tokens > 0)
+        return fail(STRIDE_ERR_INVALID_ARG, "kl_full needs logp_s as well");
     if (L.n_tokens > 0) {
         if (!teacher_logits) return fail(STRIDE_ERR_INVALID_ARG, "teacher_logits is NULL");
         for (int d = 0; d < n_teachers; ++d) {
@@ -151,8 +153,12 @@ stride_status stride_score(const stride_layout *layout, int32_t vocab, int64_t l
         e = launch_row_domain(L, n_teachers, row_dom, dev_flags, stream);
         if (e != hipSuccess) return hip_fail(e, "row-domain launch");
     }
-    e = launch_score_rows(dtype, tp, n_teachers, row_dom, student_logits, token_ids, logp_t,
-                          logp_s, L.n_tokens, vocab, ld, dev_flags, stream);
+    if (kl_full)
+        e = launch_score_pairs(dtype, tp, n_teachers, row_dom, student_logits, token_ids, logp_t,
+                               logp_s, kl_full, L.n_tokens, vocab, ld, dev_flags, stream);
+    else
+        e = launch_score_rows(dtype, tp, n_teachers, row_dom, student_logits, token_ids, logp_t,
+                              logp_s, L.n_tokens, vocab, ld, dev_flags, stream);
     if (e != hipSuccess) return hip_fail(e, "row-scoring launch");
     e = launch_turn_mean(L, logp_t, logp_s, kl, turn_mean, dev_flags, stream);
     if (e != hipSuccess) return hip_fail(e, "turn-mean launch");

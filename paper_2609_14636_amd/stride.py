@@ -54,7 +54,8 @@ def _load():
     lp = ctypes.POINTER(_CLayout)
     lib.stride_workspace_size.argtypes = [lp, i32]
     lib.stride_workspace_size.restype = sz
-    lib.stride_score.argtypes = [lp, i32, i64, i32, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+    lib.stride_score.argtypes = [lp, i32, i64, i32, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp,
+                                 sz, vp]
     lib.stride_score.restype = i32
     lib.stride_score_fused.argtypes = [lp, i32, i32, vp, vp, vp, i64, vp, vp, vp, vp, vp, vp, vp,
                                        sz, vp]
@@ -145,7 +146,8 @@ def stride_fused_workspace_size(layout: Layout, vocab: int) -> int:
 def stride_score(layout: Layout, vocab: int, teacher_logits: Sequence[torch.Tensor],
                  student_logits: torch.Tensor | None, token_ids: torch.Tensor, logp_t: torch.Tensor,
                  logp_s: torch.Tensor | None, kl: torch.Tensor | None, turn_mean: torch.Tensor,
-                 dev_flags: torch.Tensor | None, ws: torch.Tensor | None, stream=None) -> None:
+                 dev_flags: torch.Tensor | None, ws: torch.Tensor | None, stream=None,
+                 kl_full: torch.Tensor | None = None) -> None:
     t0 = teacher_logits[0]
     if t0.dim() != 2 or t0.stride(1) != 1:
         raise ValueError("teacher logits must be 2-D with unit column stride")
@@ -156,7 +158,7 @@ def stride_score(layout: Layout, vocab: int, teacher_logits: Sequence[torch.Tens
     _check(_lib.stride_score(layout.c(), int(vocab), t0.stride(0), _dtype_code(t0),
                              len(teacher_logits), ctypes.cast(ptrs, ctypes.c_void_p),
                              _ptr(student_logits), _ptr(token_ids), _ptr(logp_t), _ptr(logp_s),
-                             _ptr(kl), _ptr(turn_mean), _ptr(dev_flags), _ptr(ws),
+                             _ptr(kl), _ptr(kl_full), _ptr(turn_mean), _ptr(dev_flags), _ptr(ws),
                              0 if ws is None else ws.numel() * ws.element_size(), _stream(stream)))
 
 
@@ -204,13 +206,15 @@ class Path:
     current stream with no host synchronisation; outputs stay on the device."""
 
     def __init__(self, layout: Layout, unit: int, with_student: bool = True,
-                 device: str | torch.device = "cuda", fused_vocab: int | None = None):
+                 device: str | torch.device = "cuda", fused_vocab: int | None = None,
+                 exact_kl: bool = False):
         self.layout, self.unit = layout, unit
         n, t, r = layout.n_tokens, layout.n_turns, layout.n_rollouts
         f32 = dict(dtype=torch.float32, device=device)
         self.logp_t = torch.empty(n, **f32)
         self.logp_s = torch.empty(n, **f32) if with_student else None
         self.kl = torch.empty(n, **f32) if with_student else None
+        self.kl_full = torch.empty(n, **f32) if (with_student and exact_kl) else None
         self.turn_mean = torch.empty(t, dtype=torch.float64, device=device)
         self.cum = torch.empty(layout.n_units(unit), dtype=torch.float64, device=device)
         i32 = dict(dtype=torch.int32, device=device)
@@ -232,7 +236,7 @@ class Path:
 
     def score(self, vocab, teachers, student, token_ids, stream=None):
         stride_score(self.layout, vocab, teachers, student, token_ids, self.logp_t, self.logp_s,
-                     self.kl, self.turn_mean, self.flags, self.ws, stream)
+                     self.kl, self.turn_mean, self.flags, self.ws, stream, kl_full=self.kl_full)
 
     def score_fused(self, vocab, hidden, w, student, token_ids, stream=None):
         stride_score_fused(self.layout, vocab, hidden, w, student, token_ids, self.logp_t,
@@ -253,8 +257,9 @@ class Path:
         self.restart(alpha, correct_mask, stream)
 
     def host(self) -> dict:
-        out = {k: getattr(self, k) for k in ("logp_t", "logp_s", "kl", "turn_mean", "cum",
-                                             "stop_unit", "retained", "k_star", "k0", "k_max")}
+        out = {k: getattr(self, k) for k in ("logp_t", "logp_s", "kl", "kl_full", "turn_mean",
+                                             "cum", "stop_unit", "retained", "k_star", "k0",
+                                             "k_max")}
         res = {k: (None if v is None else v.cpu().numpy()) for k, v in out.items()}
         res["flags"] = int(self.flags.cpu().item()) & 0xFFFFFFFF
         return res

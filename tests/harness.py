@@ -117,12 +117,13 @@ def oracle_fused_scores(wl: W.Workload, rows, w_dv=None, threads: int = 16):
     return {"logp_t": lt, "logp_s": ls, "kl": OP.O.token_kl(ls, lt), "flags": ft | fs}, w_dv
 
 
-def run_gpu(wl: W.Workload, lam, alpha, inp=None, with_student=True):
+def run_gpu(wl: W.Workload, lam, alpha, inp=None, with_student=True, exact_kl=False):
     import torch
     import paper_2609_14636_amd as P
 
     inp = inp or device_inputs(wl, with_student)
-    path = P.Path(inp["layout"], wl.unit, with_student=inp["student"] is not None)
+    path = P.Path(inp["layout"], wl.unit, with_student=inp["student"] is not None,
+                  exact_kl=exact_kl)
     path.run(wl.vocab, inp["teachers"], inp["student"], inp["ids"], lam, alpha,
              start_unit=inp["start"], correct_mask=inp["mask"])
     torch.cuda.synchronize()
@@ -131,14 +132,18 @@ def run_gpu(wl: W.Workload, lam, alpha, inp=None, with_student=True):
 
 # ---------------------------------------------------------------- oracle per rollout
 
-def oracle_scores(wl: W.Workload, rollouts, threads: int = 16, with_student: bool = True):
-    """Oracle log-probabilities of the rows of the given rollouts: {r: dict(logp_t, logp_s, kl)}."""
+def oracle_scores(wl: W.Workload, rollouts, threads: int = 16, with_student: bool = True,
+                  exact_kl: bool = False):
+    """Oracle log-probabilities of the rows of the given rollouts: {r: dict(logp_t, logp_s, kl)}
+    (and kl_full, the full-vocabulary KL, when exact_kl)."""
     out = {}
     for r in rollouts:
         a, b = wl.rollout_rows(r)
         t = wl.teacher_rows_host(a, b - a, threads)
         s = wl.student_rows_host(a, b - a, threads) if with_student else None
         res = OP.score(t, s, wl.tok[a:b], wl.vocab)
+        if exact_kl:
+            res["kl_full"] = OP.O.exact_kl(t, s, wl.vocab)
         del t, s
         out[r] = res
     return out
