@@ -209,6 +209,8 @@ def main():
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--exact-kl", action="store_true",
                     help="also compute the exact full-vocabulary KL per token (paired kernel)")
+    ap.add_argument("--opd-grad", action="store_true",
+                    help="also run the OPD loss gradient (stride_opd_grad) in each step")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="only run a plain elementwise copy (torch.neg on float32) reading and "
                          "writing BYTES each per dispatch, to calibrate the HBM byte counters; keep "
@@ -250,10 +252,21 @@ def main():
     stream = torch.cuda.current_stream()
     torch.cuda.synchronize()
 
+    grad = torch.empty_like(inp["student"]) if args.opd_grad else None
+    loss = torch.empty(wl.n_tokens, dtype=torch.float32, device="cuda") if args.opd_grad else None
+    gev = []
+
     def step():
         path.score(wl.vocab, inp["teachers"], inp["student"], inp["ids"])
         path.stop(lam, inp["start"])
         path.restart(alpha, inp["mask"])
+        if args.opd_grad:
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            path.grad(wl.vocab, inp["student"], inp["ids"], grad, loss, inp["start"],
+                      scale=1.0 / wl.n_tokens)
+            e1.record(stream)
+            gev.append((e0, e1))
 
     for _ in range(args.warmup):
         step()
@@ -264,12 +277,20 @@ def main():
           for _ in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
+    gev.clear()
     for i in range(args.steps):
         ev[i][0].record(stream)
         path.score(wl.vocab, inp["teachers"], inp["student"], inp["ids"])
         ev[i][1].record(stream)
         path.stop(lam, inp["start"])
         path.restart(alpha, inp["mask"])
+        if args.opd_grad:
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            path.grad(wl.vocab, inp["student"], inp["ids"], grad, loss, inp["start"],
+                      scale=1.0 / wl.n_tokens)
+            e1.record(stream)
+            gev.append((e0, e1))
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     ms_step = (t1 - t0) * 1e3 / args.steps
@@ -309,6 +330,16 @@ def main():
                                 else "score_rows_kernel<bf16>"), "kernel_ms": score_ms,
                      "bytes_per_launch": bytes_alg},
     }
+    if args.opd_grad:
+        g_ms = sum(a.elapsed_time(b) for a, b in gev) / len(gev)
+        uoff = wl.unit_off()
+        kept = int(out["retained"].sum())
+        gbytes = kept * 2 * wl.vocab * wl.esize + (n_tok - kept) * wl.vocab * wl.esize + 13 * n_tok
+        res["opd_grad"] = {"kernel_ms": g_ms, "retained_rows": kept,
+                           "bytes_per_launch": gbytes, "achieved_GBs": gbytes / (g_ms * 1e-3) / 1e9,
+                           "frac": gbytes / (g_ms * 1e-3) / 1e9 / HBM_PEAK_GBS}
+        log(f"[bench] OPD gradient {g_ms:.3f} ms, {kept}/{n_tok} rows retained, "
+            f"{res['opd_grad']['achieved_GBs']:.0f} GB/s")
     if not args.no_cpu:
         log("[bench] timing the float64 oracle on a bounded sample")
         res["cpu_baseline"] = cpu_baseline(wl, lam, alpha, args.cpu_seconds)

@@ -191,6 +191,30 @@ stride_status stride_restart_turn(const stride_layout *layout, int32_t unit, con
                                   const uint8_t *correct_mask, int32_t *k_star, int32_t *k0,
                                   int32_t *k_max, uint32_t *dev_flags, hipStream_t stream);
 
+/*
+ * Token-level OPD loss and its gradient with respect to the student's logits,
+ * Eq. (2) (Sec. 3.1): L = -scale * sum_t log pi_S(y_t) r_t 1_trainable(t), with
+ * r_t = log pi_T(y_t) - log pi_S(y_t) held constant.  The trainable rows are the
+ * retained ones: units start_unit[r] .. stop_unit[r] of each rollout (to its last
+ * unit without a stop), the trigger included (Sec. 4.1, Algorithm 1).  For those
+ * rows  grad[t, v] = scale * r_t * (pi_S(v) - [v = y_t]);  other rows get zeros.
+ * pi_S comes from the row and log pi_S(y_t): LSE_S = s_y - log pi_S(y_t).
+ *
+ *   unit              STRIDE_UNIT_TURN or STRIDE_UNIT_TOKEN, as given to stride_stop
+ *   student_logits    [N, ld] (dtype as in stride_score), read once per retained row
+ *   logp_t, logp_s    [N] from stride_score
+ *   start_unit        [R] K0 or NULL => 0;  stop_unit  [R] from stride_stop or NULL => none
+ *   scale             multiplies loss and gradient (e.g. 1 / number of retained rows)
+ *   grad              [N, ld] output, same dtype as the logits; columns >= vocab untouched
+ *   loss              [N] float output (0 on rows that are not retained) or NULL
+ *   ws                at least stride_workspace_size(layout, unit) bytes
+ */
+stride_status stride_opd_grad(const stride_layout *layout, int32_t unit, int32_t vocab, int64_t ld,
+                              int32_t dtype, const void *student_logits, const int32_t *token_ids,
+                              const float *logp_t, const float *logp_s, const int32_t *start_unit,
+                              const int32_t *stop_unit, float scale, void *grad, float *loss,
+                              uint32_t *dev_flags, void *ws, size_t ws_bytes, hipStream_t stream);
+
 /* Message for the last non-OK status returned on this thread ("" if none). */
 const char *stride_last_error(void);
 

@@ -278,3 +278,51 @@ int oracle_fused_logp(int64_t n_rows, int64_t d, int64_t vocab, const uint16_t *
     }
     return flags;
 }
+
+/*
+ * Token-level OPD loss and its gradient with respect to the student's logits,
+ * Eq. (2) (Sec. 3.1): L = -scale * sum_t mask_t r_t log pi_S(y_t), where r_t
+ * (Eq. 1, passed in) is held constant and mask_t marks the trainable rows.
+ * Differentiating the log-softmax, d log pi_S(y) / d s_v = [v = y] - pi_S(v),
+ * so grad[t, v] = -scale mask_t r_t ([v = y_t] - pi_S(v)) and
+ * loss[t] = -scale mask_t r_t log pi_S(y_t).  pi_S is recomputed from the
+ * row itself.  grad is [n_rows, vocab] (dense, no padding); rows with
+ * mask 0 are all zero.  Returns the OR of flags as oracle_logp_rows.
+ */
+int oracle_opd_grad(int64_t n_rows, int64_t vocab, int64_t ld, int dtype, const void *student,
+                    const int32_t *ids, const double *r, const uint8_t *mask, double scale,
+                    double *grad, double *loss) {
+    int flags = 0;
+    const char *base = (const char *)student;
+    int64_t es = elem_size(dtype);
+#pragma omp parallel for schedule(dynamic, 4) reduction(| : flags)
+    for (int64_t i = 0; i < n_rows; ++i) {
+        double *g = grad + i * vocab;
+        if (!mask[i]) {
+            for (int64_t v = 0; v < vocab; ++v) g[v] = 0.0;
+            loss[i] = 0.0;
+            continue;
+        }
+        const void *row = base + i * ld * es;
+        double m, log_s;
+        int ok = row_lse(row, dtype, vocab, &m, &log_s);
+        int32_t y = ids[i];
+        if (!ok) flags |= OR_NONFINITE;
+        if (y < 0 || (int64_t)y >= vocab) {
+            flags |= OR_TOKEN_OOB;
+            ok = 0;
+        }
+        if (!ok) {
+            for (int64_t v = 0; v < vocab; ++v) g[v] = NAN;
+            loss[i] = NAN;
+            continue;
+        }
+        double c = -scale * r[i];
+        for (int64_t v = 0; v < vocab; ++v) {
+            double p = exp((load_logit(row, dtype, v) - m) - log_s);
+            g[v] = c * (((int64_t)y == v ? 1.0 : 0.0) - p);
+        }
+        loss[i] = c * ((load_logit(row, dtype, y) - m) - log_s);
+    }
+    return flags;
+}

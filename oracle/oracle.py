@@ -41,6 +41,8 @@ def _bind(path: str):
     l.oracle_restart.restype = None
     l.oracle_fused_logp.argtypes = [i64, i64, i64, vp, vp, vp, vp, vp]
     l.oracle_fused_logp.restype = i32
+    l.oracle_opd_grad.argtypes = [i64, i64, i64, i32, vp, vp, vp, vp, ctypes.c_double, vp, vp]
+    l.oracle_opd_grad.restype = i32
     return l
 
 
@@ -184,3 +186,22 @@ def fused_logp(hidden: np.ndarray, w: np.ndarray, ids: np.ndarray):
     lse = np.empty(n, np.float64)
     flags = lib().oracle_fused_logp(n, d, vocab, _p(hidden), _p(w), _p(ids), _p(logp), _p(lse))
     return logp, lse, int(flags)
+
+
+def opd_grad(student: np.ndarray, ids: np.ndarray, r: np.ndarray, mask: np.ndarray, scale: float,
+             vocab: int | None = None):
+    """Token-level OPD loss and gradient w.r.t. the student logits (Eq. 2).
+    Returns (grad [n, vocab] float64, loss [n], flags)."""
+    student = np.ascontiguousarray(student)
+    n, ld = student.shape
+    vocab = ld if vocab is None else int(vocab)
+    ids = np.ascontiguousarray(ids, dtype=np.int32)
+    r = np.ascontiguousarray(r, dtype=np.float64)
+    mask = np.ascontiguousarray(mask, dtype=np.uint8)
+    if ids.shape != (n,) or r.shape != (n,) or mask.shape != (n,):
+        raise ValueError("ids, r and mask need one entry per row")
+    grad = np.empty((n, vocab), np.float64)
+    loss = np.empty(n, np.float64)
+    flags = lib().oracle_opd_grad(n, vocab, ld, _dtype_code(student), _p(student), _p(ids), _p(r),
+                                  _p(mask), float(scale), _p(grad), _p(loss))
+    return grad, loss, int(flags)

@@ -94,3 +94,18 @@ def run(layout: Layout, teacher_rows, student_rows, ids, lam_dom, alpha_dom, uni
     s.update(r)
     s["flags"] = flags
     return s
+
+
+def retained_mask(layout: Layout, unit: int, start, stop) -> np.ndarray:
+    """Rows that join the OPD loss: units K0 .. stop of each rollout, or K0 .. last without a stop
+    (Sec. 4.1: the triggering unit is kept; Algorithm 1: the loss is on the retained tokens)."""
+    mask = np.zeros(layout.n_tokens, np.uint8)
+    unit_off, unit_tok_off = layout.units(unit)
+    for r in range(layout.n_rollouts):
+        first, n = int(unit_off[r]), int(unit_off[r + 1] - unit_off[r])
+        k0 = 0 if start is None else min(max(int(start[r]), 0), n)
+        s = int(stop[r])
+        end = s + 1 if 0 <= s < n else n
+        if end > k0:
+            mask[int(unit_tok_off[first + k0]):int(unit_tok_off[first + end])] = 1
+    return mask

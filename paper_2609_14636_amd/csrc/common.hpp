@@ -77,6 +77,13 @@ hipError_t launch_fused_teacher(const uint16_t *h, const uint16_t *w, const int3
                                 float *logp_t, int64_t n_rows, int32_t vocab, int32_t d,
                                 uint32_t *flags, void *ws, hipStream_t stream);
 
+// grad.hip
+hipError_t launch_opd_grad(const stride_layout &L, int32_t unit, int32_t dtype, int32_t vocab,
+                           int64_t ld, const void *student, const int32_t *ids,
+                           const float *logp_t, const float *logp_s, const int32_t *start,
+                           const int32_t *stop, float scale, void *grad, float *loss,
+                           uint32_t *flags, uint8_t *mask, hipStream_t stream);
+
 // restart.hip
 hipError_t launch_restart(const stride_layout &L, int32_t unit, const void *values,
                           const int32_t *stop_unit, const DomainTable &alpha, int32_t n_dom,

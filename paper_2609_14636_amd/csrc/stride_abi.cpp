@@ -268,4 +268,40 @@ stride_status stride_restart_turn(const stride_layout *layout, int32_t unit, con
     return ok();
 }
 
+stride_status stride_opd_grad(const stride_layout *layout, int32_t unit, int32_t vocab, int64_t ld,
+                              int32_t dtype, const void *student_logits, const int32_t *token_ids,
+                              const float *logp_t, const float *logp_s, const int32_t *start_unit,
+                              const int32_t *stop_unit, float scale, void *grad, float *loss,
+                              uint32_t *dev_flags, void *ws, size_t ws_bytes, hipStream_t stream) {
+    stride_status st = check_layout(layout);
+    if (st != STRIDE_OK) return st;
+    const stride_layout &L = *layout;
+    if (unit != STRIDE_UNIT_TURN && unit != STRIDE_UNIT_TOKEN)
+        return fail(STRIDE_ERR_INVALID_ARG, "unit %d is neither STRIDE_UNIT_TURN nor STRIDE_UNIT_TOKEN",
+                    unit);
+    if (vocab < 1) return fail(STRIDE_ERR_INVALID_ARG, "vocab = %d < 1", vocab);
+    if (ld < vocab) return fail(STRIDE_ERR_INVALID_ARG, "ld = %lld < vocab = %d", (long long)ld, vocab);
+    if (dtype != STRIDE_BF16 && dtype != STRIDE_F32)
+        return fail(STRIDE_ERR_UNSUPPORTED, "dtype %d is neither STRIDE_BF16 nor STRIDE_F32", dtype);
+    const int64_t esize = dtype == STRIDE_BF16 ? 2 : 4;
+    if ((ld * esize) % 16 != 0)
+        return fail(STRIDE_ERR_UNSUPPORTED, "row stride %lld bytes is not a multiple of 16",
+                    (long long)(ld * esize));
+    if (L.n_tokens > 0) {
+        if (!student_logits || !grad || !token_ids || !logp_t || !logp_s)
+            return fail(STRIDE_ERR_INVALID_ARG, "student_logits, grad, token_ids, logp_t and logp_s are required");
+        if (!aligned(student_logits, 16) || !aligned(grad, 16))
+            return fail(STRIDE_ERR_UNSUPPORTED, "student_logits and grad must be 16-byte aligned");
+    }
+    st = check_ws(layout, 0, ws, ws_bytes);
+    if (st != STRIDE_OK) return st;
+    const WsLayout w = ws_layout(L.n_rollouts, L.n_tokens, 0, 0);
+    uint8_t *mask = static_cast<uint8_t *>(ws) + w.row_dom;
+    const hipError_t e = launch_opd_grad(L, unit, dtype, vocab, ld, student_logits, token_ids,
+                                         logp_t, logp_s, start_unit, stop_unit, scale, grad, loss,
+                                         dev_flags, mask, stream);
+    if (e != hipSuccess) return hip_fail(e, "gradient launch");
+    return ok();
+}
+
 }  // extern "C"

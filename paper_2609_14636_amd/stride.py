@@ -66,6 +66,9 @@ def _load():
     lib.stride_stop.restype = i32
     lib.stride_restart_turn.argtypes = [lp, i32, vp, vp, vp, i32, vp, vp, vp, vp, vp, vp]
     lib.stride_restart_turn.restype = i32
+    lib.stride_opd_grad.argtypes = [lp, i32, i32, i64, i32, vp, vp, vp, vp, vp, vp, ctypes.c_float,
+                                    vp, vp, vp, vp, sz, vp]
+    lib.stride_opd_grad.restype = i32
     lib.stride_last_error.argtypes = []
     lib.stride_last_error.restype = ctypes.c_char_p
     return lib
@@ -199,6 +202,20 @@ def stride_restart_turn(layout: Layout, unit: int, values: torch.Tensor,
                                     _ptr(dev_flags), _stream(stream)))
 
 
+def stride_opd_grad(layout: Layout, unit: int, vocab: int, student_logits: torch.Tensor,
+                    token_ids: torch.Tensor, logp_t: torch.Tensor, logp_s: torch.Tensor,
+                    start_unit: torch.Tensor | None, stop_unit: torch.Tensor | None, scale: float,
+                    grad: torch.Tensor, loss: torch.Tensor | None, dev_flags: torch.Tensor | None,
+                    ws: torch.Tensor, stream=None) -> None:
+    if grad.dtype != student_logits.dtype or grad.stride() != student_logits.stride():
+        raise ValueError("grad must match the student logits' dtype and strides")
+    _check(_lib.stride_opd_grad(layout.c(), unit, int(vocab), student_logits.stride(0),
+                                _dtype_code(student_logits), _ptr(student_logits), _ptr(token_ids),
+                                _ptr(logp_t), _ptr(logp_s), _ptr(start_unit), _ptr(stop_unit),
+                                float(scale), _ptr(grad), _ptr(loss), _ptr(dev_flags), _ptr(ws),
+                                ws.numel() * ws.element_size(), _stream(stream)))
+
+
 class Path:
     """Output buffers and workspace for one layout, and the three calls in order.
 
@@ -249,6 +266,12 @@ class Path:
     def restart(self, alpha, correct_mask=None, stream=None):
         stride_restart_turn(self.layout, self.unit, self.values(), self.stop_unit, alpha,
                             correct_mask, self.k_star, self.k0, self.k_max, self.flags, stream)
+
+    def grad(self, vocab, student, token_ids, grad, loss=None, start_unit=None, scale=1.0,
+             stream=None):
+        stride_opd_grad(self.layout, self.unit, vocab, student, token_ids, self.logp_t,
+                        self.logp_s, start_unit, self.stop_unit, scale, grad, loss, self.flags,
+                        self.ws, stream)
 
     def run(self, vocab, teachers, student, token_ids, lam, alpha, start_unit=None,
             correct_mask=None, stream=None):

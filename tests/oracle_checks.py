@@ -313,3 +313,53 @@ ALL_CHECKS = [
     check_restart_brute_force,
     check_fused_against_matmul,
 ]
+
+
+# ---------------------------------------------------------------- OPD loss gradient (Eq. 2)
+
+def _opd_loss(x, ids, r, mask, scale):
+    """L(s) = -scale * sum_t mask_t r_t log pi_S(y_t), evaluated with the oracle's log-softmax."""
+    lp, _, _ = O.logp_rows(x, ids)
+    return -scale * float(np.sum(mask * r * lp))
+
+
+def check_opd_grad_finite_differences():
+    """The gradient equals central finite differences of the loss of Eq. (2) (with r held
+    constant), rows with mask 0 have zero gradient and loss, and every row sums to zero."""
+    rng = np.random.default_rng(37)
+    n, vocab = 5, 7
+    x = rng.normal(0, 2, size=(n, vocab))
+    ids = rng.integers(0, vocab, size=n).astype(np.int32)
+    r = rng.normal(0, 3, size=n)
+    mask = np.array([1, 0, 1, 1, 0], np.uint8)
+    scale = 0.37
+    g, loss, flags = O.opd_grad(x, ids, r, mask, scale)
+    assert flags == 0
+    h = 1e-5
+    for i in range(n):
+        for v in range(vocab):
+            xp, xm = x.copy(), x.copy()
+            xp[i, v] += h
+            xm[i, v] -= h
+            fd = (_opd_loss(xp, ids, r, mask, scale) - _opd_loss(xm, ids, r, mask, scale)) / (2 * h)
+            assert abs(g[i, v] - fd) < 1e-7, (i, v, g[i, v], fd)
+    lp, _, _ = O.logp_rows(x, ids)
+    assert np.allclose(loss, -scale * mask * r * lp, rtol=0, atol=1e-14)
+    assert np.all(g[mask == 0] == 0.0) and np.all(loss[mask == 0] == 0.0)
+    assert np.allclose(g.sum(axis=1), 0.0, atol=1e-14)
+    # descent raises the sampled logit when the teacher likes the token more (r > 0)
+    for i in np.nonzero(mask)[0]:
+        assert np.sign(g[i, ids[i]]) == -np.sign(r[i])
+
+
+def check_retained_mask():
+    """Retained rows: units K0 .. stop inclusive (turn and token units), K0 .. end without a stop."""
+    from oracle import pipeline as OP
+    lay = OP.Layout(np.array([0, 3, 5], np.int32), np.array([0, 2, 5, 6, 8, 9], np.int64))
+    m = OP.retained_mask(lay, OP.UNIT_TURN, np.array([1, 0]), np.array([1, -1]))
+    assert m.tolist() == [0, 0, 1, 1, 1, 0, 1, 1, 1]
+    m = OP.retained_mask(lay, OP.UNIT_TOKEN, np.array([2, 0]), np.array([3, 1]))
+    assert m.tolist() == [0, 0, 1, 1, 0, 0, 1, 1, 0]
+
+
+ALL_CHECKS += [check_opd_grad_finite_differences, check_retained_mask]

@@ -52,6 +52,13 @@ MUTANTS = [
     ("K0 one past k*", "k0[r] = best > 0 ? best : 0;", "k0[r] = best + 1;"),
     ("lm_head read transposed", "const uint16_t *wrow = w + k * vocab;\n                for (int64_t v = 0; v < vocab; ++v) z[v] += h * bf16_bits_to_double(wrow[v]);",
      "for (int64_t v = 0; v < vocab; ++v) z[v] += h * bf16_bits_to_double(w[v * d + k]);"),
+    ("gradient sign flipped", "double c = -scale * r[i];", "double c = scale * r[i];"),
+    ("gradient drops the sampled-token term", "g[v] = c * (((int64_t)y == v ? 1.0 : 0.0) - p);",
+     "g[v] = c * (-p);"),
+    ("gradient ignores the mask", "        if (!mask[i]) {\n            for (int64_t v = 0; v < vocab; ++v) g[v] = 0.0;",
+     "        if (0) {\n            for (int64_t v = 0; v < vocab; ++v) g[v] = 0.0;"),
+    ("gradient probability without the normaliser", "double p = exp((load_logit(row, dtype, v) - m) - log_s);",
+     "double p = exp(load_logit(row, dtype, v) - m);"),
     ("projection skips a hidden unit", "for (int64_t k = 0; k < d; ++k) {\n                double h",
      "for (int64_t k = 1; k < d; ++k) {\n                double h"),
 ]
