@@ -172,6 +172,33 @@ stride_status stride_stop(const stride_layout *layout, int32_t unit, const void 
                           uint32_t *dev_flags, void *ws, size_t ws_bytes, hipStream_t stream);
 
 /*
+ * Online form of the stop test, for use while rollouts are being generated
+ * (Algorithm 1's inner loop: after each new turn the teacher scores it and the
+ * sum over the new turns is tested against lambda, Eq. 5).  Each call appends new
+ * units to some rollouts and updates their stop state in place; feeding a
+ * rollout's units in any split gives the stride_stop result for the whole rollout.
+ *
+ *   n_active          number of rollouts receiving units in this call
+ *   slot              [n_active] int32 state index of each (0 .. size of the state arrays)
+ *   new_off           [n_active+1] int64 CSR offsets into values
+ *   unit, values      STRIDE_UNIT_TURN: double turn means (from stride_score on the
+ *                     new turns); STRIDE_UNIT_TOKEN: float teacher log-probabilities
+ *   domain            [slots] int32 or NULL => 0;  lambda (host) [n_dom]
+ *   state_cum         [slots] double, running sum over the new units (0 at the start)
+ *   state_units       [slots] int32, local index of the next unit (K0 at the start)
+ *   stop_unit         [slots] int32, -1 while running; set to the local index of
+ *                     the triggering unit, after which the rollout ignores new units
+ * The caller initialises the three state arrays for a rollout before its first
+ * call; slots not named in a call are untouched.  Calls naming the same slot twice
+ * race.
+ */
+stride_status stride_stop_step(int32_t n_active, const int32_t *slot, const int64_t *new_off,
+                               int32_t unit, const void *values, const int32_t *domain,
+                               const double *lambda, int32_t n_dom, double *state_cum,
+                               int32_t *state_units, int32_t *stop_unit, uint32_t *dev_flags,
+                               hipStream_t stream);
+
+/*
  * Prefix-buffer restart pick (Sec. 4.2 steps 1-3, Eq. 6, Algorithm 1) from the
  * record of each rollout: its units 0 .. stop_unit[r] (all units when
  * stop_unit is NULL or stop_unit[r] = -1).  Unit u is correct iff

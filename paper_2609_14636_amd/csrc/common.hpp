@@ -84,6 +84,12 @@ hipError_t launch_opd_grad(const stride_layout &L, int32_t unit, int32_t dtype, 
                            const int32_t *stop, float scale, void *grad, float *loss,
                            uint32_t *flags, uint8_t *mask, hipStream_t stream);
 
+hipError_t launch_stop_step(int32_t n_active, const int32_t *rid, const int64_t *new_off,
+                            int32_t unit, const void *values, const int32_t *domain,
+                            const DomainTable &lambda, int32_t n_dom, double *state_cum,
+                            int32_t *state_units, int32_t *stop_unit, uint32_t *flags,
+                            hipStream_t stream);
+
 // restart.hip
 hipError_t launch_restart(const stride_layout &L, int32_t unit, const void *values,
                           const int32_t *stop_unit, const DomainTable &alpha, int32_t n_dom,

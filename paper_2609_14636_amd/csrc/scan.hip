@@ -271,7 +271,91 @@ __global__ __launch_bounds__(256) void stop_finish_kernel(StopArgs a) {
     }
 }
 
+// Online form of the stop test (Algorithm 1's inner loop while a rollout is being
+// generated): active rollout a = 0 .. n_active-1 (state slot rid[a]) receives new
+// units [new_off[a], new_off[a+1]) with the given values; they are appended at
+// local index state_units[slot] on.  One wavefront per active rollout scans them in
+// 64-unit chunks (fixed shuffle tree in double) on top of the carried sum; the
+// first crossing found (ballot, lowest lane) becomes stop_unit[slot].  A rollout
+// that has already stopped ignores further units.
+template <typename VT>
+__global__ __launch_bounds__(256) void stop_step_kernel(int32_t n_active, const int32_t *rid,
+                                                        const int64_t *new_off, const VT *values,
+                                                        const int32_t *domain, DomainTable lambda,
+                                                        int32_t n_dom, double *state_cum,
+                                                        int32_t *state_units, int32_t *stop_unit,
+                                                        uint32_t *flags) {
+    const int lane = threadIdx.x & (kWave - 1);
+    const int64_t a = (int64_t)blockIdx.x * (blockDim.x / kWave) + (threadIdx.x / kWave);
+    if (a >= n_active) return;
+    const int32_t slot = rid[a];
+    if (slot < 0) {
+        if (lane == 0) raise_flag(flags, STRIDE_FLAG_BAD_OFFSETS);
+        return;
+    }
+    const int64_t b0 = new_off[a], b1 = new_off[a + 1];
+    if (b1 < b0 || b0 < 0) {
+        if (lane == 0) raise_flag(flags, STRIDE_FLAG_BAD_OFFSETS);
+        return;
+    }
+    const int32_t d = domain ? domain[slot] : 0;
+    if (d < 0 || d >= n_dom) {
+        if (lane == 0) raise_flag(flags, STRIDE_FLAG_BAD_DOMAIN);
+        return;
+    }
+    const double lam = lambda.v[d];
+    int32_t stop = stop_unit[slot];
+    double carry = state_cum[slot];
+    const int32_t u0 = state_units[slot];
+    if (stop < 0) {
+        for (int64_t c = b0; c < b1; c += kWave) {
+            const int64_t i = c + lane;
+            double v = (i < b1) ? (double)values[i] : 0.0;
+            // inclusive scan of the chunk, fixed association
+#pragma unroll
+            for (int off = 1; off < kWave; off <<= 1) {
+                const double t = __shfl_up(v, off, kWave);
+                if (lane >= off) v += t;
+            }
+            const double cum = carry + v;
+            const bool cross = (i < b1) && (cum < lam);
+            const uint64_t hit = __ballot(cross);
+            if (hit) {
+                const int first = __builtin_ctzll(hit);
+                stop = u0 + (int32_t)(c - b0) + first;
+                carry = __shfl(cum, first, kWave);
+                break;
+            }
+            const int last = (int)((b1 - c) < kWave ? (b1 - c) : kWave) - 1;
+            carry = __shfl(cum, last, kWave);
+        }
+    }
+    if (lane == 0) {
+        state_cum[slot] = carry;
+        state_units[slot] = u0 + (int32_t)(b1 - b0);
+        stop_unit[slot] = stop;
+    }
+}
+
 }  // namespace
+
+hipError_t launch_stop_step(int32_t n_active, const int32_t *rid, const int64_t *new_off,
+                            int32_t unit, const void *values, const int32_t *domain,
+                            const DomainTable &lambda, int32_t n_dom, double *state_cum,
+                            int32_t *state_units, int32_t *stop_unit, uint32_t *flags,
+                            hipStream_t stream) {
+    if (n_active == 0) return hipSuccess;
+    const unsigned blocks = (unsigned)((n_active + 3) / 4);
+    if (unit == STRIDE_UNIT_TURN)
+        hipLaunchKernelGGL(stop_step_kernel<double>, dim3(blocks), dim3(256), 0, stream, n_active,
+                           rid, new_off, static_cast<const double *>(values), domain, lambda, n_dom,
+                           state_cum, state_units, stop_unit, flags);
+    else
+        hipLaunchKernelGGL(stop_step_kernel<float>, dim3(blocks), dim3(256), 0, stream, n_active,
+                           rid, new_off, static_cast<const float *>(values), domain, lambda, n_dom,
+                           state_cum, state_units, stop_unit, flags);
+    return hipGetLastError();
+}
 
 hipError_t launch_stop(const stride_layout &L, int32_t unit, const void *values,
                        const DomainTable &lambda, int32_t n_dom, const int32_t *start,

@@ -244,6 +244,27 @@ stride_status stride_stop(const stride_layout *layout, int32_t unit, const void 
     return ok();
 }
 
+stride_status stride_stop_step(int32_t n_active, const int32_t *slot, const int64_t *new_off,
+                               int32_t unit, const void *values, const int32_t *domain,
+                               const double *lambda, int32_t n_dom, double *state_cum,
+                               int32_t *state_units, int32_t *stop_unit, uint32_t *dev_flags,
+                               hipStream_t stream) {
+    if (n_active < 0) return fail(STRIDE_ERR_INVALID_ARG, "n_active = %d < 0", n_active);
+    if (unit != STRIDE_UNIT_TURN && unit != STRIDE_UNIT_TOKEN)
+        return fail(STRIDE_ERR_INVALID_ARG, "unit %d is neither STRIDE_UNIT_TURN nor STRIDE_UNIT_TOKEN",
+                    unit);
+    stride_status st = check_domains(lambda, n_dom, "lambda");
+    if (st != STRIDE_OK) return st;
+    if (n_active > 0 && (!slot || !new_off || !values || !state_cum || !state_units || !stop_unit))
+        return fail(STRIDE_ERR_INVALID_ARG, "slot, new_off, values and the state arrays are required");
+    DomainTable lt{};
+    for (int i = 0; i < n_dom; ++i) lt.v[i] = lambda[i];
+    const hipError_t e = launch_stop_step(n_active, slot, new_off, unit, values, domain, lt, n_dom,
+                                          state_cum, state_units, stop_unit, dev_flags, stream);
+    if (e != hipSuccess) return hip_fail(e, "stop-step launch");
+    return ok();
+}
+
 stride_status stride_restart_turn(const stride_layout *layout, int32_t unit, const void *values,
                                   const int32_t *stop_unit, const double *alpha, int32_t n_dom,
                                   const uint8_t *correct_mask, int32_t *k_star, int32_t *k0,

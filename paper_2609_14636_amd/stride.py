@@ -69,6 +69,8 @@ def _load():
     lib.stride_opd_grad.argtypes = [lp, i32, i32, i64, i32, vp, vp, vp, vp, vp, vp, ctypes.c_float,
                                     vp, vp, vp, vp, sz, vp]
     lib.stride_opd_grad.restype = i32
+    lib.stride_stop_step.argtypes = [i32, vp, vp, i32, vp, vp, vp, i32, vp, vp, vp, vp, vp]
+    lib.stride_stop_step.restype = i32
     lib.stride_last_error.argtypes = []
     lib.stride_last_error.restype = ctypes.c_char_p
     return lib
@@ -188,6 +190,17 @@ def stride_stop(layout: Layout, unit: int, values: torch.Tensor, lam: Sequence[f
                             len(lam), _ptr(start_unit), _ptr(cum), _ptr(stop_unit),
                             _ptr(n_retained_tokens), _ptr(dev_flags), _ptr(ws),
                             ws.numel() * ws.element_size(), _stream(stream)))
+
+
+def stride_stop_step(slot: torch.Tensor, new_off: torch.Tensor, unit: int, values: torch.Tensor,
+                     domain: torch.Tensor | None, lam: Sequence[float], state_cum: torch.Tensor,
+                     state_units: torch.Tensor, stop_unit: torch.Tensor,
+                     dev_flags: torch.Tensor | None, stream=None) -> None:
+    lt = _doubles(lam)
+    _check(_lib.stride_stop_step(slot.numel(), _ptr(slot), _ptr(new_off), unit, _ptr(values),
+                                 _ptr(domain), ctypes.cast(lt, ctypes.c_void_p), len(lam),
+                                 _ptr(state_cum), _ptr(state_units), _ptr(stop_unit),
+                                 _ptr(dev_flags), _stream(stream)))
 
 
 def stride_restart_turn(layout: Layout, unit: int, values: torch.Tensor,

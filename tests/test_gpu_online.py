@@ -1,0 +1,137 @@
+"""Online stop test (stride_stop_step): units arrive a turn or a chunk at a time.
+
+Feeding a rollout's units in any split must give the batch decision of Eq. (5): the
+same stop index as the oracle's stop over the whole rollout (exact unless the
+oracle's cumulative value passes within 1e-3 of lambda), and the carried sum at the
+stop equal to the oracle's cumulative value there.
+"""
+import sys
+
+import numpy as np
+import pytest
+
+from synth import workloads as W
+from tests import harness as H
+
+pytestmark = pytest.mark.gpu
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(autouse=True)
+def _gpu():
+    import torch
+    assert torch.cuda.is_available()
+    yield
+    torch.cuda.synchronize()
+
+
+@pytest.mark.parametrize("unit,seed", [(0, 0), (1, 1), (1, 2)])
+def test_online_matches_batch_on_host_values(unit, seed):
+    import torch
+    import paper_2609_14636_amd as P
+    g = np.random.default_rng(seed)
+    R = 37
+    sizes = g.integers(1, 12 if unit == 0 else 5000, size=R)
+    off = np.zeros(R + 1, np.int64)
+    off[1:] = np.cumsum(sizes)
+    U = int(off[-1])
+    vals = -np.abs(g.normal(1.0, 0.7, size=U))
+    if unit == 1:  # token units arrive as float32 log-probabilities; both sides get those values
+        vals = vals.astype(np.float32).astype(np.float64)
+    dom = g.integers(0, 2, size=R).astype(np.int32)
+    start = (g.random(R) * sizes * 0.3).astype(np.int32)
+    lam = [-4.0, -9.0] if unit == 0 else [-900.0, -2500.0]
+    cum_o, stop_o, _ = H.OP.O.stop(off, vals, np.array(lam)[dom], start)
+    dt = torch.float64 if unit == 0 else torch.float32
+    # state: K0 units reused, nothing summed yet, running
+    st_cum = torch.zeros(R, dtype=torch.float64, device="cuda")
+    st_units = torch.from_numpy(start.copy()).cuda()
+    st_stop = torch.full((R,), -1, dtype=torch.int32, device="cuda")
+    flags = torch.zeros(1, dtype=torch.int32, device="cuda")
+    dom_d = torch.from_numpy(dom).cuda()
+    pos = start.astype(np.int64).copy()  # next local unit to feed per rollout
+    steps = 0
+    while True:
+        active = [r for r in range(R) if pos[r] < sizes[r] and g.random() < 0.8]
+        if not any(pos[r] < sizes[r] for r in range(R)):
+            break
+        if not active:
+            continue
+        chunks, slot = [], []
+        for r in active:
+            n = int(min(sizes[r] - pos[r], 1 if unit == 0 else g.integers(1, 700)))
+            chunks.append(vals[off[r] + pos[r]:off[r] + pos[r] + n])
+            slot.append(r)
+            pos[r] += n
+        new_off = np.zeros(len(chunks) + 1, np.int64)
+        new_off[1:] = np.cumsum([c.size for c in chunks])
+        v = torch.from_numpy(np.concatenate(chunks)).to(dt).cuda()
+        P.stride_stop_step(torch.tensor(slot, dtype=torch.int32).cuda(),
+                           torch.from_numpy(new_off).cuda(), unit, v, dom_d, lam, st_cum,
+                           st_units, st_stop, flags)
+        steps += 1
+    torch.cuda.synchronize()
+    assert int(flags.item()) == 0
+    s = st_stop.cpu().numpy()
+    c = st_cum.cpu().numpy()
+    for r in range(R):
+        if s[r] != stop_o[r]:
+            a = off[r]
+            hi = sizes[r] if (s[r] < 0 or stop_o[r] < 0) else max(s[r], stop_o[r]) + 1
+            assert np.any(np.abs(cum_o[a + start[r]:a + hi] - lam[dom[r]]) <= H.BAND), r
+        elif s[r] >= 0:
+            want = cum_o[off[r] + s[r]]
+            assert abs(c[r] - want) <= 1e-9 * max(abs(want), 1.0), (r, c[r], want)
+    assert np.array_equal(st_units.cpu().numpy(), sizes)
+    say(f"[online unit={unit}] {steps} calls, stops equal {int(np.sum(s == stop_o))}/{R}")
+
+
+def test_online_turn_by_turn_scoring_matches_batch_path():
+    """Score each new turn as it is generated (its rows gathered into a fresh buffer, as a
+    rollout engine would hand them over), then step the stop test: the final stops equal
+    the batch path's."""
+    import torch
+    import paper_2609_14636_amd as P
+    wl = W.make("agentic", seed=1007, scale=dict(R=4, turns=6, tok_lo=40, tok_hi=120, vocab=8192))
+    sc = H.oracle_scores(wl, range(wl.n_rollouts))
+    lam, alpha = H.thresholds(wl, sc)
+    inp = H.device_inputs(wl)
+    batch = P.Path(inp["layout"], W.UNIT_TURN)
+    batch.run(wl.vocab, inp["teachers"], inp["student"], inp["ids"], lam, alpha)
+    torch.cuda.synchronize()
+    R, K = wl.n_rollouts, 6
+    st_cum = torch.zeros(R, dtype=torch.float64, device="cuda")
+    st_units = torch.zeros(R, dtype=torch.int32, device="cuda")
+    st_stop = torch.full((R,), -1, dtype=torch.int32, device="cuda")
+    flags = torch.zeros(1, dtype=torch.int32, device="cuda")
+    teacher = inp["teachers"][0]
+    for k in range(K):
+        stop_now = st_stop.cpu().numpy()
+        active = [r for r in range(R) if stop_now[r] < 0]   # stopped rollouts generate nothing
+        if not active:
+            break
+        rows = []
+        for r in active:
+            t = int(wl.rollout_turn_off[r]) + k
+            rows.append(np.arange(wl.turn_tok_off[t], wl.turn_tok_off[t + 1]))
+        lens = [x.size for x in rows]
+        idx = torch.from_numpy(np.concatenate(rows)).cuda()
+        t_new = teacher[idx].contiguous()
+        ids_new = inp["ids"][idx].contiguous()
+        tto = np.zeros(len(active) + 1, np.int64)
+        tto[1:] = np.cumsum(lens)
+        lay = P.Layout(torch.arange(len(active) + 1, dtype=torch.int32).cuda(),
+                       torch.from_numpy(tto).cuda(), int(tto[-1]))
+        step = P.Path(lay, W.UNIT_TURN, with_student=False)
+        step.score(wl.vocab, [t_new], None, ids_new)
+        P.stride_stop_step(torch.tensor(active, dtype=torch.int32).cuda(),
+                           torch.arange(len(active) + 1, dtype=torch.int64).cuda(), W.UNIT_TURN,
+                           step.turn_mean, None, lam, st_cum, st_units, st_stop, flags)
+    torch.cuda.synchronize()
+    assert int(flags.item()) == 0
+    assert st_stop.cpu().numpy().tolist() == batch.stop_unit.cpu().numpy().tolist()
+    say(f"[online turn-by-turn] stops {st_stop.cpu().numpy().tolist()}")
