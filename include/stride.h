@@ -242,6 +242,32 @@ stride_status stride_opd_grad(const stride_layout *layout, int32_t unit, int32_t
                               const int32_t *stop_unit, float scale, void *grad, float *loss,
                               uint32_t *dev_flags, void *ws, size_t ws_bytes, hipStream_t stream);
 
+/*
+ * Per-task trajectory record H(x) of the prefix buffer (Algorithm 1), kept on
+ * the host.  After a rollout of task x, put() stores its per-unit values (turn
+ * means, or token log-probabilities in the single-turn setting) and optional
+ * correctness mask, replacing the previous record.  Before the next rollout,
+ * plan() returns for each task the restart pick of Sec. 4.2 / Eq. (6) on its
+ * record -- K_max (leading correct run, value > alpha and mask set), k* (lowest
+ * index of its minimum, -1 if K_max = 0) and K0 = max(k*, 0) units of reused
+ * context -- or k* = -1, K0 = 0, K_max = 0 for a task without a record.
+ * All pointers here are host pointers.  The store is an object the caller
+ * creates and destroys (host memory only); its calls are thread-safe.
+ * get() copies up to `capacity` values (and mask bytes, 1 where none was
+ * stored) and returns the record length, or -1 if the task has none.
+ */
+typedef struct stride_records stride_records;
+stride_records *stride_records_create(void);
+void stride_records_destroy(stride_records *rec);
+stride_status stride_records_put(stride_records *rec, int64_t task, int32_t n_units,
+                                 const double *values, const uint8_t *mask);
+int32_t stride_records_get(stride_records *rec, int64_t task, int32_t capacity, double *values,
+                           uint8_t *mask);
+int64_t stride_records_size(stride_records *rec);
+stride_status stride_records_plan(stride_records *rec, int32_t n_tasks, const int64_t *tasks,
+                                  const double *alpha, int32_t *k_star, int32_t *k0,
+                                  int32_t *k_max);
+
 /* Message for the last non-OK status returned on this thread ("" if none). */
 const char *stride_last_error(void);
 

@@ -71,6 +71,18 @@ def _load():
     lib.stride_opd_grad.restype = i32
     lib.stride_stop_step.argtypes = [i32, vp, vp, i32, vp, vp, vp, i32, vp, vp, vp, vp, vp]
     lib.stride_stop_step.restype = i32
+    lib.stride_records_create.argtypes = []
+    lib.stride_records_create.restype = vp
+    lib.stride_records_destroy.argtypes = [vp]
+    lib.stride_records_destroy.restype = None
+    lib.stride_records_put.argtypes = [vp, i64, i32, vp, vp]
+    lib.stride_records_put.restype = i32
+    lib.stride_records_get.argtypes = [vp, i64, i32, vp, vp]
+    lib.stride_records_get.restype = i32
+    lib.stride_records_size.argtypes = [vp]
+    lib.stride_records_size.restype = i64
+    lib.stride_records_plan.argtypes = [vp, i32, vp, vp, vp, vp, vp]
+    lib.stride_records_plan.restype = i32
     lib.stride_last_error.argtypes = []
     lib.stride_last_error.restype = ctypes.c_char_p
     return lib
@@ -227,6 +239,57 @@ def stride_opd_grad(layout: Layout, unit: int, vocab: int, student_logits: torch
                                 _ptr(logp_t), _ptr(logp_s), _ptr(start_unit), _ptr(stop_unit),
                                 float(scale), _ptr(grad), _ptr(loss), _ptr(dev_flags), _ptr(ws),
                                 ws.numel() * ws.element_size(), _stream(stream)))
+
+
+class Records:
+    """Host-side per-task trajectory record H(x) (Algorithm 1) held by libstride.so."""
+
+    def __init__(self):
+        self._h = _lib.stride_records_create()
+        if not self._h:
+            raise MemoryError("stride_records_create failed")
+
+    def close(self):
+        if self._h:
+            _lib.stride_records_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        self.close()
+
+    def __len__(self):
+        return int(_lib.stride_records_size(self._h))
+
+    def put(self, task: int, values, mask=None):
+        import numpy as np
+        v = np.ascontiguousarray(values, dtype=np.float64)
+        m = None if mask is None else np.ascontiguousarray(mask, dtype=np.uint8)
+        st = _lib.stride_records_put(self._h, int(task), v.size, v.ctypes.data,
+                                     None if m is None else m.ctypes.data)
+        if st != STRIDE_OK:
+            raise StrideError(st, "stride_records_put")
+
+    def get(self, task: int):
+        import numpy as np
+        n = _lib.stride_records_get(self._h, int(task), 0, None, None)
+        if n < 0:
+            return None
+        v = np.empty(n, np.float64)
+        m = np.empty(n, np.uint8)
+        _lib.stride_records_get(self._h, int(task), n, v.ctypes.data, m.ctypes.data)
+        return v, m
+
+    def plan(self, tasks, alpha):
+        """(k_star, k0, k_max) per task, 0-based; tasks without a record get (-1, 0, 0)."""
+        import numpy as np
+        t = np.ascontiguousarray(tasks, dtype=np.int64)
+        a = np.ascontiguousarray(np.broadcast_to(np.asarray(alpha, np.float64), t.shape))
+        ks, k0, km = (np.empty(t.size, np.int32) for _ in range(3))
+        st = _lib.stride_records_plan(self._h, t.size, t.ctypes.data, a.ctypes.data,
+                                      ks.ctypes.data, k0.ctypes.data, km.ctypes.data)
+        if st != STRIDE_OK:
+            raise StrideError(st, "stride_records_plan")
+        return ks, k0, km
 
 
 class Path:
