@@ -6,16 +6,19 @@
 // log pi_T(y) = z_y - log sum_v exp(z_v).  The [N, V] logits (40 GB at the
 // fused workload) exist only tile by tile in registers.
 //
-// Kernel 1 (MFMA): a 256 x 256 tile of z per workgroup, K = d streamed in
-//   64-wide blocks through double-buffered LDS (rows padded by 16 B), four
-//   waves in a 2 x 2 grid each holding a 128 x 128 fp32 accumulator (16
-//   v_mfma_f32_32x32x16_bf16 tiles); the fragments of the next 16-wide k step
-//   are read while the current one multiplies.  Both operands are
-//   K-contiguous, so each MFMA operand is one 16-byte LDS read.  W is the A
+// Kernel 1 (MFMA): a 256 x 256 tile of z per workgroup, four waves in a 2 x 2
+//   grid each holding a 128 x 128 fp32 accumulator (16 v_mfma_f32_32x32x16_bf16
+//   tiles, 256 accumulation registers).  K = d streams through a ring of five
+//   32-wide LDS stages filled by direct global->LDS loads (global_load_lds_dwordx4,
+//   no register staging), issued four stages ahead; rows are XOR-swizzled so the
+//   16-byte fragment reads are free of bank conflicts.  The fragments of stage
+//   k+1 are read while stage k multiplies, and the instruction order is pinned so
+//   LDS reads and global loads issue in the shadow of the MFMAs.  Both operands
+//   are K-contiguous, so each MFMA operand is one 16-byte LDS read.  W is the A
 //   operand and H the B operand, so each lane's accumulators hold 64 of one
-//   token's 128 logits and its partner lane (l ^ 32) the other 64: the
-//   epilogue reduces a token to (max, sum of exp(z - max)) with one exchange
-//   and writes it to a partial table [V/128][N] (tokens contiguous).
+//   token's 128 logits and its partner lane (l ^ 32) the other 64: the epilogue
+//   reduces a token to (max, sum of exp(z - max)) with one exchange and writes it
+//   to a partial table [V/128][N] (tokens contiguous).
 //   Workgroups are numbered so that the 32 resident on one XCD (dispatch is
 //   round-robin over the 8 XCDs) cover a 4 x 8 block of tiles of a 16 x 16
 //   super-tile, and super-tiles advance along V: each XCD's L2 serves every
@@ -33,11 +36,16 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
-constexpr int kBM = 256, kBN = 256, kBK = 64;
-constexpr int kRowPad = kBK + 8;                    // bf16 per LDS row (16 B pad)
-constexpr int kStageElems = 2 * kBM * kRowPad;      // A and B of one stage
-constexpr size_t kLdsBytes = 2 * kStageElems * 2;   // two stages, bf16
-constexpr int kHalf = 128;                          // columns per partial
+#define GLOBAL_PTR(p) ((const __attribute__((address_space(1))) void *)(p))
+#define LDS_PTR(p) ((__attribute__((address_space(3))) void *)(p))
+
+constexpr int kBM = 256, kBN = 256, kBK = 32;
+constexpr int kStages = 5;                          // LDS ring depth
+constexpr int kRowB = kBK * 2;                      // 64 bytes per LDS row
+constexpr int kTileB = kBM * kRowB;                 // 16 KB per operand tile
+constexpr int kStageB = 2 * kTileB;                 // 32 KB per stage
+constexpr size_t kLdsBytes = (size_t)kStages * kStageB;
+constexpr int kHalf = 128;                          // vocabulary entries per partial
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.69314718055994531f;
 
@@ -54,10 +62,22 @@ struct FusedArgs {
 
 __device__ __forceinline__ float ex2(float x) { return __builtin_amdgcn_exp2f(x); }
 
+// 16-byte chunk c of LDS row r is stored at position c ^ swz(r).  Rows are 64 B, so a
+// wave's 32 fragment rows at one chunk would otherwise fall on the same banks; with
+// this swizzle any 8 (or 16) consecutive rows hit distinct 16-byte bank groups.
+__device__ __forceinline__ int swz(int r) { return ((r >> 1) ^ (r >> 3)) & 3; }
+
+// Wait until at most N vector-memory operations of this wave are outstanding.
+template <int N>
+__device__ __forceinline__ void wait_vmem() {
+    __builtin_amdgcn_s_waitcnt((N & 0xF) | (7 << 4) | (0xF << 8) | ((N >> 4) << 14));
+}
+
 __global__ __launch_bounds__(256, 1) void fused_lse_kernel(FusedArgs a) {
-    extern __shared__ __attribute__((aligned(16))) uint16_t lds[];
+    extern __shared__ __attribute__((aligned(1024))) char lds[];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int wm = wave >> 1, wn = wave & 1;
+    // wave (wv, wt): vocabulary half wv, token half wt of the 256 x 256 tile
+    const int wt = wave >> 1, wv = wave & 1;
 
     // ---- tile of this workgroup (XCD-aware order) ----
     const int b = blockIdx.x;
@@ -68,38 +88,71 @@ __global__ __launch_bounds__(256, 1) void fused_lse_kernel(FusedArgs a) {
     if (tm >= a.tiles_m || tn >= a.tiles_n) return;
     const int64_t m0 = (int64_t)tm * kBM;
     const int64_t n0 = (int64_t)tn * kBN;
-    const int d = a.d;
+    const int d = a.d, nk = d / kBK;
 
-    // ---- global -> register staging: thread owns 8 A and 8 B 16-byte chunks ----
-    const int crow = tid >> 3, ckc = tid & 7;  // chunk row within a 32-row slab, k chunk
-    const u32x4 zero4 = {0u, 0u, 0u, 0u};
-    u32x4 ra[8], rb[8];
-    auto load_block = [&](int k0) {
+    // ---- direct global -> LDS loads: each wave fills 64 rows of each operand per stage,
+    // 16 rows per instruction (lane l -> row l >> 2, position l & 3 of the swizzled row).
+    // Rows past N or V read a valid row; their results are never used.
+    const int lq = lane >> 2, lp = lane & 3;
+    const uint16_t *hsrc[4], *wsrc[4];
 #pragma unroll
-        for (int i = 0; i < 8; ++i) {
-            const int64_t r = m0 + crow + 32 * i;
-            ra[i] = (r < a.n_rows)
-                        ? *reinterpret_cast<const u32x4 *>(a.h + r * d + k0 + ckc * 8)
-                        : zero4;
-            const int64_t c = n0 + crow + 32 * i;
-            rb[i] = (c < a.vocab)
-                        ? *reinterpret_cast<const u32x4 *>(a.w + c * d + k0 + ckc * 8)
-                        : zero4;
+    for (int i = 0; i < 4; ++i) {
+        const int R = 64 * wave + 16 * i + lq;
+        const int c = lp ^ swz(R);
+        int64_t hr = m0 + R;
+        if (hr >= a.n_rows) hr = a.n_rows - 1;
+        int64_t wr = n0 + R;
+        if (wr >= a.vocab) wr = a.vocab - 1;
+        hsrc[i] = a.h + hr * d + c * 8;
+        wsrc[i] = a.w + wr * d + c * 8;
+    }
+    // Every step issues exactly one stage (8 loads per wave); a stage past the end reloads
+    // stage nk-1 into the buffer that has just retired, which is never read again, so the
+    // number of loads in flight is the same at every wait.
+    auto issue = [&](int k) {
+        if (k >= nk) k = nk - 1;
+        char *st = lds + (k % kStages) * kStageB;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            __builtin_amdgcn_global_load_lds(GLOBAL_PTR(hsrc[i] + k * kBK),
+                                             LDS_PTR(st + (64 * wave + 16 * i) * kRowB), 16, 0, 0);
+            __builtin_amdgcn_global_load_lds(GLOBAL_PTR(wsrc[i] + k * kBK),
+                                             LDS_PTR(st + kTileB + (64 * wave + 16 * i) * kRowB),
+                                             16, 0, 0);
         }
     };
-    auto store_block = [&](int stage) {
-        uint16_t *As = lds + stage * kStageElems;
-        uint16_t *Bs = As + kBM * kRowPad;
-#pragma unroll
-        for (int i = 0; i < 8; ++i) {
-            *reinterpret_cast<u32x4 *>(As + (crow + 32 * i) * kRowPad + ckc * 8) = ra[i];
-            *reinterpret_cast<u32x4 *>(Bs + (crow + 32 * i) * kRowPad + ckc * 8) = rb[i];
-        }
+    // Stage k+1 has landed in every wave's share once each wave has at most
+    // (kStages - 3) stages outstanding and all waves meet at the barrier.
+    auto sync_stages = [&](int allowed) {
+        if (allowed >= 3) wait_vmem<24>();
+        else if (allowed == 2) wait_vmem<16>();
+        else if (allowed == 1) wait_vmem<8>();
+        else wait_vmem<0>();
+        __builtin_amdgcn_sched_barrier(0);
+        __builtin_amdgcn_s_barrier();
+        __builtin_amdgcn_sched_barrier(0);
     };
 
-    // acc[i][j]: vocabulary 32-block i of this wave's 128 entries x token 32-block j of its
-    // 128 tokens.  With W as the MFMA A operand and H as B, lane l holds token j*32 + l%32
-    // and 16 vocabulary entries of it, so a row's reduction stays inside a lane pair.
+    // ---- MFMA fragments: W is the A operand and H the B operand, so lane l's accumulators
+    // hold token j*32 + l%32 and 16 vocabulary entries of it.  Fragments of stage k+1 are
+    // read into the other register buffer while stage k multiplies.
+    const int fr = lane & 31, fh = lane >> 5;
+    int foff[2];
+#pragma unroll
+    for (int kq = 0; kq < 2; ++kq) foff[kq] = fr * kRowB + (((2 * kq + fh) ^ swz(fr)) * 16);
+    bf16x8 F[2][2][2][4];  // [register buffer][k step][W, H][32-row block]
+    auto read_frags = [&](int k, int buf) {
+        const char *st = lds + (k % kStages) * kStageB;
+        const char *Ws = st + kTileB + (wv * 128) * kRowB;
+        const char *Hs = st + (wt * 128) * kRowB;
+#pragma unroll
+        for (int kq = 0; kq < 2; ++kq)
+#pragma unroll
+            for (int t = 0; t < 4; ++t) {
+                F[buf][kq][0][t] = *reinterpret_cast<const bf16x8 *>(Ws + t * 32 * kRowB + foff[kq]);
+                F[buf][kq][1][t] = *reinterpret_cast<const bf16x8 *>(Hs + t * 32 * kRowB + foff[kq]);
+            }
+    };
     f32x16 acc[4][4];
 #pragma unroll
     for (int i = 0; i < 4; ++i)
@@ -107,46 +160,45 @@ __global__ __launch_bounds__(256, 1) void fused_lse_kernel(FusedArgs a) {
         for (int j = 0; j < 4; ++j)
 #pragma unroll
             for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.0f;
-
-    const int nk = d / kBK;
-    load_block(0);
-    store_block(0);
-    __syncthreads();
-    const int frag_row = lane & 31, frag_k = 8 * (lane >> 5);
-    // wave (wv, wt): vocabulary half wv, token half wt of the 256 x 256 tile
-    const int wv = wn, wt = wm;
-    for (int kb = 0; kb < nk; ++kb) {
-        if (kb + 1 < nk) load_block((kb + 1) * kBK);
-        const uint16_t *Hs = lds + (kb & 1) * kStageElems + (wt * 128) * kRowPad;
-        const uint16_t *Ws = lds + (kb & 1) * kStageElems + kBM * kRowPad + (wv * 128) * kRowPad;
-        bf16x8 fw[2][4], fh[2][4];
-#pragma unroll
-        for (int t = 0; t < 4; ++t) {
-            fw[0][t] = *reinterpret_cast<const bf16x8 *>(Ws + (t * 32 + frag_row) * kRowPad + frag_k);
-            fh[0][t] = *reinterpret_cast<const bf16x8 *>(Hs + (t * 32 + frag_row) * kRowPad + frag_k);
+    auto step = [&](int k, int cur, bool prefetch) {
+        if (prefetch) {
+            sync_stages(kStages - 3);
+            issue(k + kStages - 1);
+            read_frags(k + 1, cur ^ 1);
         }
 #pragma unroll
-        for (int kq = 0; kq < kBK / 16; ++kq) {
-            const int cur = kq & 1;
-            if (kq + 1 < kBK / 16) {
-#pragma unroll
-                for (int t = 0; t < 4; ++t) {
-                    fw[cur ^ 1][t] = *reinterpret_cast<const bf16x8 *>(
-                        Ws + (t * 32 + frag_row) * kRowPad + (kq + 1) * 16 + frag_k);
-                    fh[cur ^ 1][t] = *reinterpret_cast<const bf16x8 *>(
-                        Hs + (t * 32 + frag_row) * kRowPad + (kq + 1) * 16 + frag_k);
-                }
-            }
+        for (int kq = 0; kq < 2; ++kq)
 #pragma unroll
             for (int i = 0; i < 4; ++i)
 #pragma unroll
                 for (int j = 0; j < 4; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fw[cur][i], fh[cur][j],
-                                                                        acc[i][j], 0, 0, 0);
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(F[cur][kq][0][i],
+                                                                        F[cur][kq][1][j], acc[i][j],
+                                                                        0, 0, 0);
+        if (prefetch) {
+            // interleave: {MFMA, LDS read, MFMA, LDS read, MFMA, global load, MFMA} x 8
+#pragma unroll
+            for (int g = 0; g < 8; ++g) {
+                __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+                __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+                __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+                __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+                __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+                __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+                __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+            }
         }
-        if (kb + 1 < nk) store_block((kb + 1) & 1);
-        __syncthreads();
+    };
+#pragma unroll
+    for (int p = 0; p < kStages - 1; ++p) issue(p);
+    sync_stages(kStages - 2);  // stage 0 has landed
+    read_frags(0, 0);
+    for (int kb = 0; kb + 2 < nk; kb += 2) {  // nk is even: pairs keep the buffers static
+        step(kb, 0, true);
+        step(kb + 1, 1, true);
     }
+    step(nk - 2, 0, true);
+    step(nk - 1, 1, false);
 
     // ---- epilogue: per token of this wave, (max, sum exp(z - max)) over its 128 entries ----
     const int half = lane >> 5;
