@@ -128,7 +128,7 @@ stride_status stride_score(const stride_layout *layout, int32_t vocab, int64_t l
  * the matrix cores (bf16 inputs, fp32 accumulation).  The student's logits
  * are given as in stride_score.
  *
- *   d                hidden size, a positive multiple of 64
+ *   d                hidden size, a multiple of 64 in [64, 65536]
  *   hidden_t         [N, d] bf16 row-major, 16-byte aligned
  *   w_t              [vocab, d] bf16 row-major (a linear layer's weight: row v
  *                    holds the weights of vocabulary entry v), 16-byte aligned

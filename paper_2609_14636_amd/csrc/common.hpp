@@ -39,6 +39,9 @@ struct WsLayout {
 constexpr int kScanThreads = 256;
 constexpr int kScanItems = 8;
 constexpr int64_t kScanTile = (int64_t)kScanThreads * kScanItems;
+// Largest hidden size of the fused projection: a 256-row operand tile (256 * d * 2
+// bytes) must fit the 32-bit range of one buffer descriptor.
+constexpr int32_t kMaxFusedD = 65536;
 
 WsLayout ws_layout(int64_t n_rollouts, int64_t n_tokens, int64_t n_units, int64_t fused_partials);
 

@@ -13,7 +13,7 @@
 //   group multiplies from registers, the other reads its next fragments from LDS
 //   and issues loads, then a barrier swaps them (ping-pong), so each SIMD's matrix
 //   unit always has a wave with work.  K = d streams through two 64-wide LDS
-//   stages filled by direct global->LDS loads (global_load_lds_dwordx4, no
+//   stages filled by direct buffer->LDS loads (buffer_load_dwordx4 ... lds, no
 //   register staging); eight lanes load one row's 128 bytes, a whole cache line,
 //   and rows are XOR-swizzled so the 16-byte fragment reads are free of bank
 //   conflicts.  Both operands are K-contiguous, so each MFMA operand is one
@@ -38,7 +38,6 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
-#define GLOBAL_PTR(p) ((const __attribute__((address_space(1))) void *)(p))
 #define LDS_PTR(p) ((__attribute__((address_space(3))) void *)(p))
 
 constexpr int kBM = 256, kBN = 256, kBK = 64;      // tile and LDS stage width
@@ -51,6 +50,9 @@ constexpr size_t kLdsBytes = (size_t)kStages * kStageB;
 constexpr int kHalf = 128;                         // vocabulary entries per partial
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.69314718055994531f;
+// Third word of a raw buffer descriptor: 32-bit data format, no swizzle; accesses
+// at or beyond num_records bytes return zeros.
+constexpr int kBufferFlags = 0x00020000;
 
 struct FusedArgs {
     const uint16_t *h;     // [N, d]
@@ -108,31 +110,33 @@ __global__ __launch_bounds__(kThreads, 1) void fused_lse_kernel(FusedArgs a) {
     const int64_t n0 = (int64_t)tn * kBN;
     const int d = a.d, ns = d / kBK;
 
-    // ---- direct global -> LDS loads: each wave fills 32 rows of each operand per
-    // stage, 8 rows per instruction (lane l -> row l >> 3, position l & 7 of the
-    // swizzled row).  Rows past N or V read a valid row; their results are unused.
+    // ---- direct global -> LDS loads (buffer_load_dwordx4 ... lds): each wave fills 32
+    // rows of each operand per stage, 8 rows per instruction (lane l -> row l >> 3,
+    // position l & 7 of the swizzled row).  Each operand's descriptor spans only the
+    // rows of this tile that exist, so rows past N or V read as zeros (their results
+    // are never used) and no load can leave the operand.  Lane offsets are 32-bit and
+    // shared by both operands; the K position goes in the scalar offset.
+    const int64_t h_rows = (a.n_rows - m0) < kBM ? (a.n_rows - m0) : kBM;
+    const int64_t w_rows = (a.vocab - n0) < kBN ? (a.vocab - n0) : kBN;
+    const __amdgpu_buffer_rsrc_t rh = __builtin_amdgcn_make_buffer_rsrc(
+        (void *)(a.h + m0 * d), (short)0, (int)(h_rows * d * 2), kBufferFlags);
+    const __amdgpu_buffer_rsrc_t rw = __builtin_amdgcn_make_buffer_rsrc(
+        (void *)(a.w + n0 * d), (short)0, (int)(w_rows * d * 2), kBufferFlags);
     const int lr = lane >> 3, lp = lane & 7;
-    const uint16_t *hsrc[4], *wsrc[4];
+    int voff[4];
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
         const int R = 32 * wave + 8 * i + lr;
-        const int c = lp ^ swz(R);
-        int64_t hr = m0 + R;
-        if (hr >= a.n_rows) hr = a.n_rows - 1;
-        int64_t wr = n0 + R;
-        if (wr >= a.vocab) wr = a.vocab - 1;
-        hsrc[i] = a.h + hr * d + c * 8;
-        wsrc[i] = a.w + wr * d + c * 8;
+        voff[i] = (R * d + ((lp ^ swz(R)) * 8)) * 2;
     }
     auto issue = [&](int j) {
         char *st = lds + (j & 1) * kStageB;
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-            __builtin_amdgcn_global_load_lds(GLOBAL_PTR(hsrc[i] + j * kBK),
-                                             LDS_PTR(st + (32 * wave + 8 * i) * kRowB), 16, 0, 0);
-            __builtin_amdgcn_global_load_lds(GLOBAL_PTR(wsrc[i] + j * kBK),
-                                             LDS_PTR(st + kTileB + (32 * wave + 8 * i) * kRowB),
-                                             16, 0, 0);
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                rh, LDS_PTR(st + (32 * wave + 8 * i) * kRowB), 16, voff[i], j * kRowB, 0, 0);
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                rw, LDS_PTR(st + kTileB + (32 * wave + 8 * i) * kRowB), 16, voff[i], j * kRowB, 0, 0);
         }
     };
 

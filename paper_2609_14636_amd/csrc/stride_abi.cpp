@@ -179,8 +179,9 @@ stride_status stride_score_fused(const stride_layout *layout, int32_t vocab, int
     if (st != STRIDE_OK) return st;
     const stride_layout &L = *layout;
     if (vocab < 1) return fail(STRIDE_ERR_INVALID_ARG, "vocab = %d < 1", vocab);
-    if (d < 64 || d % 64 != 0)
-        return fail(STRIDE_ERR_UNSUPPORTED, "hidden size d = %d is not a positive multiple of 64", d);
+    if (d < 64 || d % 64 != 0 || d > kMaxFusedD)
+        return fail(STRIDE_ERR_UNSUPPORTED,
+                    "hidden size d = %d is not a multiple of 64 in [64, %d]", d, kMaxFusedD);
     if (!student_logits && (logp_s || kl))
         return fail(STRIDE_ERR_INVALID_ARG, "logp_s / kl requested without student logits");
     if (L.n_tokens > 0) {

@@ -101,10 +101,16 @@ def test_unaligned_row_stride_is_unsupported():
     assert ei.value.status == 2
 
 
-def test_fused_variant_reports_its_status():
+@pytest.mark.parametrize("d", [32, 96, 65536 + 64])
+def test_fused_hidden_size_outside_the_supported_range_is_rejected(d):
+    """The fused projection takes d in multiples of 64 up to 65,536 (one operand tile must fit
+    a 32-bit buffer range); anything else returns STRIDE_ERR_UNSUPPORTED before any launch."""
     lay = _layout()
-    with pytest.raises(P.StrideError):
-        P.library().stride_score_fused  # exported
-        st = P.library().stride_score_fused(None, 0, 0, None, None, None, 0, None, None, None,
-                                            None, None, None, None, 0, None)
-        P.stride._check(st)
+    h = torch.zeros((10, d), dtype=torch.bfloat16)
+    w = torch.zeros((16, d), dtype=torch.bfloat16)
+    ids = torch.zeros(10, dtype=torch.int32)
+    with pytest.raises(P.StrideError) as ei:
+        P.stride_score_fused(lay, 16, h, w, None, ids, _fake(10), None, None,
+                             torch.zeros(3, dtype=torch.float64), None, None, stream=0)
+    assert ei.value.status == 2
+    assert "hidden size" in P.library().stride_last_error().decode()
