@@ -28,6 +28,7 @@ MFMA_BF16_PEAK_TFLOPS = 2500.0
 METRIC = "scored tokens/sec (logp+KL+stop scan) and % of HBM peak, 1 MI355X"
 PARAMS = os.path.join(ROOT, "tests", "golden", "workload_params.json")
 TRAFFIC = os.path.join(ROOT, "profiles", "traffic.json")
+FUSED_SRC = os.path.join(ROOT, "paper_2609_14636_amd", "csrc", "fused.hip")
 SCORE_SRC = os.path.join(ROOT, "paper_2609_14636_amd", "csrc", "score.hip")
 
 
@@ -45,14 +46,21 @@ def workload_params(name: str, seed: int):
     return [float(x) for x in e["lambda"]], [float(x) for x in e["alpha"]]
 
 
-def source_digest() -> str:
-    with open(SCORE_SRC, "rb") as f:
+def source_digest(path: str = None) -> str:
+    with open(path or SCORE_SRC, "rb") as f:
         return hashlib.sha256(f.read()).hexdigest()[:16]
 
 
-def measured_traffic(workload: str):
-    """HBM bytes per launch of the scoring kernel from committed rocprofv3 counters, if they were
-    taken on the current kernel source; else None.
+def shape_label(wl) -> str:
+    """'R rollouts x K turns' with K per rollout (or its range when rollouts differ)."""
+    per = np.diff(np.asarray(wl.rollout_turn_off))
+    k = f"{int(per.min())}" if per.min() == per.max() else f"{int(per.min())}-{int(per.max())}"
+    return f"{wl.n_rollouts} rollouts x {k} turns ({wl.n_turns} turns)"
+
+
+def measured_traffic(workload: str, kernel_src: str = None, key: str = "score_hip_sha256_16"):
+    """HBM bytes per launch of the dominant kernel from committed rocprofv3 counters, if they
+    were taken on the current kernel source; else None.
 
     FETCH_SIZE and WRITE_SIZE (KiB per dispatch) are each scaled by the ratio of known bytes to
     the same counter's reading on a one-dispatch plain copy (torch.neg on float32)."""
@@ -61,7 +69,7 @@ def measured_traffic(workload: str):
     with open(TRAFFIC) as f:
         t = json.load(f)
     e = t.get(workload)
-    if not e or e.get("score_hip_sha256_16") != source_digest():
+    if not e or e.get(key) != source_digest(kernel_src):
         return None
     c = t["copy_calibration"]
     k_fetch = c["bytes"] / (c["fetch_kib"] * 1024.0)
@@ -179,14 +187,17 @@ def bench_fused(args):
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_step,
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
         "data": "synthetic",
-        "config": {"workload": f"fused: {wl.n_rollouts} rollouts x {wl.n_turns} turns, "
+        "config": {"workload": f"fused: {shape_label(wl)}, "
                                f"{wl.n_tokens} scored tokens, teacher logits h W on the fly "
                                f"(d={wl.fused_d}, V={wl.vocab}), student logits bf16",
                    "global_batch": wl.n_rollouts, "seq_len": wl.n_tokens // wl.n_rollouts,
                    "parallelism": "single GPU"},
         "roofline": {"bound": "mfma", "achieved": achieved, "peak": MFMA_BF16_PEAK_TFLOPS,
-                     "unit": "TFLOP/s", "frac": achieved / MFMA_BF16_PEAK_TFLOPS, "traffic": None,
-                     "kernel": "fused_lse_kernel (bf16 MFMA 32x32x16)", "kernel_ms": k_ms,
+                     "unit": "TFLOP/s", "frac": achieved / MFMA_BF16_PEAK_TFLOPS,
+                     "traffic": measured_traffic("fused", FUSED_SRC, "fused_hip_sha256_16"),
+                     "kernel": "fused_lse_kernel (bf16 MFMA 32x32x16); kernel_ms brackets the "
+                               "teacher call (projection + per-row gather + merge)",
+                     "kernel_ms": k_ms,
                      "flops_per_launch": flops},
     }
     if not args.no_cpu:
@@ -320,7 +331,7 @@ def main():
         "vs_baseline": None,
         "dtype": "bf16" if wl.dtype == W.BF16 else "f32",
         "data": "synthetic",
-        "config": {"workload": f"{args.workload}: {wl.n_rollouts} rollouts x {wl.n_turns} turns, "
+        "config": {"workload": f"{args.workload}: {shape_label(wl)}, "
                                f"{n_tok} scored tokens, V={wl.vocab}, teacher+student logits",
                    "global_batch": wl.n_rollouts, "seq_len": int(n_tok // max(wl.n_rollouts, 1)),
                    "parallelism": "single GPU"},
