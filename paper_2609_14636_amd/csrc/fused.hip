@@ -25,10 +25,12 @@
 //   round-robin over the 8 XCDs) cover a 4 x 8 block of tiles of a 16 x 16
 //   super-tile, and super-tiles advance along V: each XCD's L2 serves every
 //   H panel slice to 8 tiles and every W slice to 4, and the 16 H panels of a
-//   super-row stay in the last-level cache while W streams past.
+//   super-row stay in the last-level cache while W streams past.  With fewer
+//   than 16 (or 8) row tiles the super-tile is 8 x 32 (or 4 x 64) tiles, so
+//   every XCD still has tiles.
 // Kernel 2: z_y = h . w_y per row (one wave per row, fp32).
-// Kernel 3: one thread per row merges its V/128 partials (reads coalesced
-//   across rows) and writes log pi_T(y) = (z_y - m) - log s.
+// Kernel 3: four waves per 64 rows merge each row's V/128 partials (reads
+//   coalesced across rows) and write log pi_T(y) = (z_y - m) - log s.
 #include "common.hpp"
 
 namespace stride {
@@ -63,6 +65,8 @@ struct FusedArgs {
     int32_t d;
     int32_t n_half;
     int32_t tiles_m, tiles_n, super_cols;
+    int32_t xcd_cols;      // XCD blocks per super-tile row: 2, 4 or 8 (the super-tile is
+                           // 32 / xcd_cols row tiles by 8 * xcd_cols vocabulary tiles)
 };
 
 __device__ __forceinline__ float ex2(float x) { return __builtin_amdgcn_exp2f(x); }
@@ -103,8 +107,9 @@ __global__ __launch_bounds__(kThreads, 1) void fused_lse_kernel(FusedArgs a) {
     const int b = blockIdx.x;
     const int xcd = b & 7, s = b >> 3;
     const int S = s >> 5, q = s & 31;
-    const int tm = (S / a.super_cols) * 16 + (xcd >> 1) * 4 + (q & 3);
-    const int tn = (S % a.super_cols) * 16 + (xcd & 1) * 8 + (q >> 2);
+    const int xc = a.xcd_cols, xr = 8 / xc;
+    const int tm = (S / a.super_cols) * (4 * xr) + (xcd / xc) * 4 + (q & 3);
+    const int tn = (S % a.super_cols) * (8 * xc) + (xcd % xc) * 8 + (q >> 2);
     if (tm >= a.tiles_m || tn >= a.tiles_n) return;
     const int64_t m0 = (int64_t)tm * kBM;
     const int64_t n0 = (int64_t)tn * kBN;
@@ -272,21 +277,47 @@ __global__ __launch_bounds__(256) void fused_gather_kernel(const uint16_t *h, co
     if (lane == 0) zy[row] = acc;
 }
 
-// Merge the V/128 partials of each row and finish log pi_T(y).
+// Fold one partial (max p.x, sum p.y of exp(z - p.x)) into a running (m, s).
+__device__ __forceinline__ void fold_partial(float &m, float &s, const float2 p) {
+    const float mn = fmaxf(m, p.x);
+    const float ref = (mn == -INFINITY) ? 0.0f : mn;
+    s = s * ex2((m - ref) * kLog2e) + p.y * ex2((p.x - ref) * kLog2e);
+    m = mn;
+}
+
+constexpr int kMergeRows = 64;   // rows per workgroup, one per lane
+constexpr int kMergeSplit = 4;   // waves per workgroup, each folding every 4th partial
+
+// Merge the V/128 partials of each row and finish log pi_T(y).  Wave w of a workgroup
+// folds partials w, w+4, w+8, ... of its 64 rows (each load is 64 consecutive rows,
+// 512 contiguous bytes, eight loads in flight); the four wave results are combined in
+// LDS in wave order, so the result does not depend on timing.
 __global__ __launch_bounds__(256) void fused_merge_kernel(const float2 *partial, const float *zy,
                                                           const int32_t *ids, float *logp_t,
                                                           int64_t n_rows, int32_t n_half,
                                                           int32_t vocab, uint32_t *flags) {
-    const int64_t row = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (row >= n_rows) return;
+    __shared__ float2 red[kMergeSplit][kMergeRows];
+    const int r = threadIdx.x & (kMergeRows - 1), sp = threadIdx.x / kMergeRows;
+    const int64_t row = (int64_t)blockIdx.x * kMergeRows + r;
     float m = -INFINITY, s = 0.0f;
-    for (int j = 0; j < n_half; ++j) {
-        const float2 p = partial[(int64_t)j * n_rows + row];
-        const float mn = fmaxf(m, p.x);
-        const float ref = (mn == -INFINITY) ? 0.0f : mn;
-        s = s * ex2((m - ref) * kLog2e) + p.y * ex2((p.x - ref) * kLog2e);
-        m = mn;
+    if (row < n_rows) {
+        const float2 *col = partial + row;
+        int j = sp;
+        constexpr int U = 8;
+        for (; j + (U - 1) * kMergeSplit < n_half; j += U * kMergeSplit) {
+            float2 p[U];
+#pragma unroll
+            for (int u = 0; u < U; ++u) p[u] = col[(int64_t)(j + u * kMergeSplit) * n_rows];
+#pragma unroll
+            for (int u = 0; u < U; ++u) fold_partial(m, s, p[u]);
+        }
+        for (; j < n_half; j += kMergeSplit) fold_partial(m, s, col[(int64_t)j * n_rows]);
     }
+    red[sp][r] = make_float2(m, s);
+    __syncthreads();
+    if (sp != 0 || row >= n_rows) return;
+#pragma unroll
+    for (int k = 1; k < kMergeSplit; ++k) fold_partial(m, s, red[k][r]);
     const int32_t y = ids[row];
     uint32_t bad = 0;
     if (!((m > -INFINITY) && (m < INFINITY) && (s > 0.0f) && (s < INFINITY))) bad |= STRIDE_FLAG_NONFINITE;
@@ -321,8 +352,12 @@ hipError_t launch_fused_teacher(const uint16_t *h, const uint16_t *w, const int3
     a.n_half = (vocab + kHalf - 1) / kHalf;
     a.tiles_m = (int)((n_rows + kBM - 1) / kBM);
     a.tiles_n = (vocab + kBN - 1) / kBN;
-    a.super_cols = (a.tiles_n + 15) / 16;
-    const int super_rows = (a.tiles_m + 15) / 16;
+    // Few row tiles (small batches): lay the eight XCD blocks out along V instead, so
+    // every XCD still gets work.
+    a.xcd_cols = a.tiles_m >= 16 ? 2 : (a.tiles_m >= 8 ? 4 : 8);
+    const int xr = 8 / a.xcd_cols;
+    a.super_cols = (a.tiles_n + 8 * a.xcd_cols - 1) / (8 * a.xcd_cols);
+    const int super_rows = (a.tiles_m + 4 * xr - 1) / (4 * xr);
     a.partial = static_cast<float2 *>(ws);
     float *zy = reinterpret_cast<float *>(static_cast<char *>(ws) +
                                           (size_t)a.n_half * n_rows * sizeof(float2));
@@ -337,7 +372,8 @@ hipError_t launch_fused_teacher(const uint16_t *h, const uint16_t *w, const int3
                        h, w, ids, zy, n_rows, vocab, d);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(fused_merge_kernel, dim3((unsigned)((n_rows + 255) / 256)), dim3(256), 0,
+    hipLaunchKernelGGL(fused_merge_kernel, dim3((unsigned)((n_rows + kMergeRows - 1) / kMergeRows)),
+                       dim3(kMergeRows * kMergeSplit), 0,
                        stream, a.partial, zy, ids, logp_t, n_rows, a.n_half, vocab, flags);
     return hipGetLastError();
 }
