@@ -318,6 +318,21 @@ def main():
     bytes_alg = per_token * n_tok
     achieved = bytes_alg / (score_ms * 1e-3) / 1e9
     traffic = None if args.exact_kl else measured_traffic(args.workload)
+    # streaming-read reference: the same rows read with the same access pattern, no arithmetic
+    sink = torch.empty(2 * n_tok, dtype=torch.int32, device="cuda")
+    read_bytes = (wl.vocab * wl.esize) // 16 * 16
+    pev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(max(args.steps // 2, 3))]
+    P.stride_probe_read(inp["teachers"][0], inp["student"], read_bytes, sink)
+    for a, b in pev:
+        a.record(stream)
+        P.stride_probe_read(inp["teachers"][0], inp["student"], read_bytes, sink)
+        b.record(stream)
+    torch.cuda.synchronize()
+    probe_ms = sum(a.elapsed_time(b) for a, b in pev) / len(pev)
+    ceiling = 2 * n_tok * read_bytes / (probe_ms * 1e-3) / 1e9
+    log(f"[bench] streaming-read reference on the same rows: {probe_ms:.3f} ms = {ceiling:.0f} GB/s; "
+        f"scoring reaches {100 * achieved / ceiling:.1f}% of it")
     res = {
         "metric": METRIC,
         "value": n_tok / (ms_step * 1e-3),
@@ -339,7 +354,10 @@ def main():
                      "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
                      "kernel": ("score_pairs_kernel<bf16> (with exact KL)" if args.exact_kl
                                 else "score_rows_kernel<bf16>"), "kernel_ms": score_ms,
-                     "bytes_per_launch": bytes_alg},
+                     "bytes_per_launch": bytes_alg,
+                     "read_ceiling": {"achieved": ceiling, "unit": "GB/s", "frac": achieved / ceiling,
+                                      "kernel": "probe_read_kernel: the same rows, same loads, "
+                                                "no arithmetic"}},
     }
     if args.opd_grad:
         g_ms = sum(a.elapsed_time(b) for a, b in gev) / len(gev)

@@ -268,6 +268,25 @@ stride_status stride_records_plan(stride_records *rec, int32_t n_tasks, const in
                                   const double *alpha, int32_t *k_star, int32_t *k0,
                                   int32_t *k_max);
 
+/* Streaming-read reference (a measurement aid, not a step of the method).
+ *
+ * Reads n_rows rows of `a` (and, when b is not NULL, the same rows of `b`,
+ * interleaved row by row) with the scoring kernel's access pattern -- one
+ * wavefront per row, 16-byte non-temporal loads -- and does no arithmetic, so
+ * timing it gives the read bandwidth that pattern reaches; the scoring kernel's
+ * bandwidth is reported as a fraction of it next to the fraction of peak.
+ *   a, b        device rows, 16-byte aligned; b may be NULL
+ *   n_rows      rows to read from each matrix (>= 0)
+ *   row_bytes   row stride in bytes, a multiple of 16
+ *   read_bytes  bytes read from the start of each row, <= row_bytes (rounded
+ *               down to a multiple of 16)
+ *   sink        [n_rows, or 2 * n_rows with b] uint32 written with an XOR of
+ *               each row's words (keeps the loads live)
+ * Errors: STRIDE_ERR_INVALID_ARG for NULL pointers or inconsistent sizes,
+ * STRIDE_ERR_UNSUPPORTED for misaligned rows. */
+stride_status stride_probe_read(const void *a, const void *b, int64_t n_rows, int64_t row_bytes,
+                                int64_t read_bytes, uint32_t *sink, hipStream_t stream);
+
 /* Message for the last non-OK status returned on this thread ("" if none). */
 const char *stride_last_error(void);
 

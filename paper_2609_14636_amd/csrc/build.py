@@ -15,7 +15,7 @@ ROOT = os.path.dirname(PKG)
 LIB = os.path.join(PKG, "libstride.so")
 BUILD = os.path.join(ROOT, "_build")
 
-SOURCES = ["stride_abi.cpp", "record.cpp", "score.hip", "turn.hip", "scan.hip", "restart.hip", "fused.hip", "grad.hip"]
+SOURCES = ["stride_abi.cpp", "record.cpp", "score.hip", "turn.hip", "scan.hip", "restart.hip", "fused.hip", "grad.hip", "probe.hip"]
 FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-Wall",
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
          "-I", os.path.join(ROOT, "include")]

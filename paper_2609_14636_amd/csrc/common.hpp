@@ -94,6 +94,8 @@ hipError_t launch_stop_step(int32_t n_active, const int32_t *rid, const int64_t 
                             hipStream_t stream);
 
 // restart.hip
+hipError_t launch_probe_read(const void *a, const void *b, int64_t n_rows, int64_t row_bytes,
+                             int64_t read_bytes, uint32_t *sink, hipStream_t stream);
 hipError_t launch_restart(const stride_layout &L, int32_t unit, const void *values,
                           const int32_t *stop_unit, const DomainTable &alpha, int32_t n_dom,
                           const uint8_t *mask, int32_t *k_star, int32_t *k0, int32_t *k_max,

@@ -326,4 +326,19 @@ stride_status stride_opd_grad(const stride_layout *layout, int32_t unit, int32_t
     return ok();
 }
 
+stride_status stride_probe_read(const void *a, const void *b, int64_t n_rows, int64_t row_bytes,
+                                int64_t read_bytes, uint32_t *sink, hipStream_t stream) {
+    if (n_rows < 0) return fail(STRIDE_ERR_INVALID_ARG, "n_rows = %lld < 0", (long long)n_rows);
+    if (n_rows == 0) return ok();
+    if (!a || !sink) return fail(STRIDE_ERR_INVALID_ARG, "a or sink is NULL");
+    if (read_bytes < 16 || read_bytes > row_bytes)
+        return fail(STRIDE_ERR_INVALID_ARG, "read_bytes = %lld outside [16, row_bytes = %lld]",
+                    (long long)read_bytes, (long long)row_bytes);
+    if (row_bytes % 16 != 0 || !aligned(a, 16) || (b && !aligned(b, 16)))
+        return fail(STRIDE_ERR_UNSUPPORTED, "rows must be 16-byte aligned");
+    hipError_t e = launch_probe_read(a, b, n_rows, row_bytes, read_bytes, sink, stream);
+    if (e != hipSuccess) return hip_fail(e, "probe launch");
+    return ok();
+}
+
 }  // extern "C"

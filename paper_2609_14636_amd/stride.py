@@ -83,6 +83,8 @@ def _load():
     lib.stride_records_size.restype = i64
     lib.stride_records_plan.argtypes = [vp, i32, vp, vp, vp, vp, vp]
     lib.stride_records_plan.restype = i32
+    lib.stride_probe_read.argtypes = [vp, vp, i64, i64, i64, vp, vp]
+    lib.stride_probe_read.restype = i32
     lib.stride_last_error.argtypes = []
     lib.stride_last_error.restype = ctypes.c_char_p
     return lib
@@ -239,6 +241,16 @@ def stride_opd_grad(layout: Layout, unit: int, vocab: int, student_logits: torch
                                 _ptr(logp_t), _ptr(logp_s), _ptr(start_unit), _ptr(stop_unit),
                                 float(scale), _ptr(grad), _ptr(loss), _ptr(dev_flags), _ptr(ws),
                                 ws.numel() * ws.element_size(), _stream(stream)))
+
+
+def stride_probe_read(a: torch.Tensor, b: torch.Tensor | None, read_bytes: int,
+                      sink: torch.Tensor, stream=None) -> None:
+    """Streaming-read reference: reads the first read_bytes of every row of a (and b) with the
+    scoring kernel's access pattern and no arithmetic (a measurement aid)."""
+    if b is not None and (b.stride() != a.stride() or b.shape != a.shape or b.dtype != a.dtype):
+        raise ValueError("a and b must share shape, dtype and strides")
+    _check(_lib.stride_probe_read(_ptr(a), _ptr(b), a.shape[0], a.stride(0) * a.element_size(),
+                                  int(read_bytes), _ptr(sink), _stream(stream)))
 
 
 class Records:

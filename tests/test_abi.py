@@ -114,3 +114,18 @@ def test_fused_hidden_size_outside_the_supported_range_is_rejected(d):
                              torch.zeros(3, dtype=torch.float64), None, None, stream=0)
     assert ei.value.status == 2
     assert "hidden size" in P.library().stride_last_error().decode()
+
+
+@pytest.mark.parametrize("case", ["read_past_row", "misaligned_stride", "null_sink"])
+def test_probe_read_argument_errors(case):
+    a = torch.zeros((4, 64), dtype=torch.bfloat16)
+    sink = torch.zeros(8, dtype=torch.int32)
+    with pytest.raises(P.StrideError) as ei:
+        if case == "read_past_row":
+            P.stride_probe_read(a, None, 129 * 2, sink, stream=0)
+        elif case == "misaligned_stride":
+            P.stride_probe_read(torch.zeros((4, 60), dtype=torch.bfloat16), None, 64, sink,
+                                stream=0)  # 120-byte rows
+        else:
+            P.stride_probe_read(a, None, 64, None, stream=0)
+    assert ei.value.status == (2 if case == "misaligned_stride" else 1)
