@@ -1,0 +1,108 @@
+"""Edge cases on the GPU: an empty batch through every entry point, data errors in the fused
+projection path, and a fused hidden size past the full-size workload's.
+
+The empty batch has nothing to compare; every call must succeed, raise no flag and write
+nothing.  The fused error rows must come back NaN with the right flags while every other row
+still matches the float64 oracle.
+"""
+import math
+import sys
+
+import numpy as np
+import pytest
+
+from synth import workloads as W
+from tests import harness as H
+
+pytestmark = pytest.mark.gpu
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(autouse=True)
+def _gpu():
+    import torch
+    assert torch.cuda.is_available()
+    yield
+    torch.cuda.synchronize()
+
+
+def test_empty_batch_every_entry_point():
+    import torch
+    import paper_2609_14636_amd as P
+    dev = "cuda"
+    lay = P.Layout(torch.zeros(1, dtype=torch.int32, device=dev),
+                   torch.zeros(1, dtype=torch.int64, device=dev), 0)
+    e = torch.empty(0, dtype=torch.float32, device=dev)
+    x = torch.empty((0, 64), dtype=torch.bfloat16, device=dev)
+    ids = torch.empty(0, dtype=torch.int32, device=dev)
+    tm = torch.empty(0, dtype=torch.float64, device=dev)
+    i32 = torch.empty(0, dtype=torch.int32, device=dev)
+    flags = torch.zeros(1, dtype=torch.int32, device=dev)
+    for unit in (P.STRIDE_UNIT_TURN, P.STRIDE_UNIT_TOKEN):
+        ws = torch.empty(P.stride_workspace_size(lay, unit), dtype=torch.uint8, device=dev)
+        vals = tm if unit == P.STRIDE_UNIT_TURN else e
+        P.stride_score(lay, 64, [x], x, ids, e, e, e, tm, flags, ws, kl_full=e)
+        P.stride_stop(lay, unit, vals, [-1.0], None, tm, i32, None, flags, ws)
+        P.stride_restart_turn(lay, unit, vals, i32, [-1.0], None, i32, i32, i32, flags)
+        P.stride_opd_grad(lay, unit, 64, x, ids, e, e, None, i32, 1.0, torch.empty_like(x), e,
+                          flags, ws)
+        P.stride_stop_step(i32, torch.zeros(1, dtype=torch.int64, device=dev), unit, vals, None,
+                           [-1.0], tm, i32, i32, flags)
+    fws = torch.empty(P.stride_fused_workspace_size(lay, 64), dtype=torch.uint8, device=dev)
+    P.stride_score_fused(lay, 64, torch.empty((0, 64), dtype=torch.bfloat16, device=dev),
+                         torch.empty((64, 64), dtype=torch.bfloat16, device=dev), x, ids, e, e, e,
+                         tm, flags, fws)
+    torch.cuda.synchronize()
+    assert int(flags.item()) == 0
+
+
+def test_fused_data_errors_flag_only_their_rows():
+    import torch
+    import paper_2609_14636_amd as P
+    wl = W.make("fused", seed=77, scale=dict(R=1, turns=2, tok=48, vocab=1000, d=128))
+    inp = H.device_inputs_fused(wl)
+    ids = inp["ids"].clone()
+    ids[3] = wl.vocab        # token id out of range
+    ids[7] = -1              # negative token id
+    hidden = inp["hidden"].clone()
+    hidden[11, 5] = float("inf")   # non-finite hidden state
+    N = wl.n_tokens
+    lt = torch.empty(N, dtype=torch.float32, device="cuda")
+    tm = torch.empty(wl.n_turns, dtype=torch.float64, device="cuda")
+    flags = torch.zeros(1, dtype=torch.int32, device="cuda")
+    ws = torch.empty(P.stride_fused_workspace_size(inp["layout"], wl.vocab), dtype=torch.uint8,
+                     device="cuda")
+    P.stride_score_fused(inp["layout"], wl.vocab, hidden, inp["w"], None, ids, lt, None, None, tm,
+                         flags, ws)
+    torch.cuda.synchronize()
+    f = int(flags.item())
+    assert f & P.STRIDE_FLAG_TOKEN_OOB and f & P.STRIDE_FLAG_NONFINITE, hex(f)
+    got = lt.cpu().numpy()
+    bad = [3, 7, 11]
+    assert np.isnan(got[bad]).all()
+    good = np.setdiff1d(np.arange(N), bad)
+    sc, _ = H.oracle_fused_scores(wl, good)
+    assert sc["flags"] == 0
+    d = np.max(np.abs(got[good] - sc["logp_t"]))
+    assert d <= H.TOL_LOGP, d
+    say(f"[fused errors] flags {f:#x}, max |d logp_t| on the other {good.size} rows {d:.2e}")
+
+
+def test_fused_wide_hidden_size():
+    """d = 4096 (64 LDS stages of the projection), a partial row tile and a ragged vocabulary."""
+    wl = W.make("fused", seed=4096, scale=dict(R=1, turns=2, tok=40, vocab=1000, d=4096))
+    sc, _ = H.oracle_fused_scores(wl, np.arange(wl.n_tokens))
+    assert sc["flags"] == 0
+    per = {0: {k: sc[k] for k in ("logp_t", "logp_s", "kl")}}
+    lam, alpha = [-math.inf], [-math.inf]
+    ora = {0: (per[0], H.oracle_rollout(wl, 0, per[0], lam, alpha))}
+    gpu = H.run_gpu_fused(wl, lam, alpha)
+    assert gpu["flags"] == 0, hex(gpu["flags"])
+    d = np.max(np.abs(gpu["logp_t"] - sc["logp_t"]))
+    assert d <= H.TOL_LOGP, d
+    rep = H.compare(wl, gpu, ora, lam, alpha)
+    say(f"[fused d=4096] max |d logp_t| {d:.2e}; {rep}")
