@@ -31,6 +31,8 @@
 // Kernel 2: z_y = h . w_y per row (one wave per row, fp32).
 // Kernel 3: four waves per 64 rows merge each row's V/128 partials (reads
 //   coalesced across rows) and write log pi_T(y) = (z_y - m) - log s.
+#include <atomic>
+
 #include "common.hpp"
 
 namespace stride {
@@ -334,6 +336,26 @@ __global__ __launch_bounds__(256) void fused_merge_kernel(const float2 *partial,
 
 }  // namespace
 
+namespace {
+
+// The projection kernel's dynamic LDS (128 KB) is above the default limit; the limit is
+// raised once per device, so later calls (and calls under stream capture) make no
+// attribute call.
+hipError_t ensure_lds_limit() {
+    static std::atomic<uint64_t> done{0};
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    const uint64_t bit = (dev >= 0 && dev < 64) ? (1ull << dev) : 0;
+    if (bit && (done.load(std::memory_order_acquire) & bit)) return hipSuccess;
+    e = hipFuncSetAttribute(reinterpret_cast<const void *>(fused_lse_kernel),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)kLdsBytes);
+    if (e == hipSuccess && bit) done.fetch_or(bit, std::memory_order_release);
+    return e;
+}
+
+}  // namespace
+
 size_t fused_ws_bytes(int64_t n_rows, int32_t vocab) {
     const int64_t n_half = ((int64_t)vocab + kHalf - 1) / kHalf;
     return (size_t)n_half * n_rows * sizeof(float2) + (size_t)n_rows * sizeof(float) + 256;
@@ -361,10 +383,10 @@ hipError_t launch_fused_teacher(const uint16_t *h, const uint16_t *w, const int3
     a.partial = static_cast<float2 *>(ws);
     float *zy = reinterpret_cast<float *>(static_cast<char *>(ws) +
                                           (size_t)a.n_half * n_rows * sizeof(float2));
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(fused_lse_kernel),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)kLdsBytes);
+    hipError_t e = ensure_lds_limit();
     if (e != hipSuccess) return e;
     const int64_t blocks = (int64_t)super_rows * a.super_cols * 256;
+    if (blocks > 0x7fffffff) return hipErrorInvalidConfiguration;  // grid past the 32-bit limit
     hipLaunchKernelGGL(fused_lse_kernel, dim3((unsigned)blocks), dim3(kThreads), kLdsBytes, stream, a);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
