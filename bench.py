@@ -318,6 +318,7 @@ def main():
     bytes_alg = per_token * n_tok
     achieved = bytes_alg / (score_ms * 1e-3) / 1e9
     traffic = None if args.exact_kl else measured_traffic(args.workload)
+    dt = "bf16" if wl.dtype == W.BF16 else "f32"
     # streaming-read reference: the same rows read with the same access pattern, no arithmetic
     sink = torch.empty(2 * n_tok, dtype=torch.int32, device="cuda")
     read_bytes = (wl.vocab * wl.esize) // 16 * 16
@@ -352,8 +353,8 @@ def main():
                    "parallelism": "single GPU"},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
-                     "kernel": ("score_pairs_kernel<bf16> (with exact KL)" if args.exact_kl
-                                else "score_rows_kernel<bf16>"), "kernel_ms": score_ms,
+                     "kernel": (f"score_pairs_kernel<{dt}> (with exact KL)" if args.exact_kl
+                                else f"score_rows_kernel<{dt}>"), "kernel_ms": score_ms,
                      "bytes_per_launch": bytes_alg,
                      "read_ceiling": {"achieved": ceiling, "unit": "GB/s", "frac": achieved / ceiling,
                                       "kernel": "probe_read_kernel: the same rows, same loads, "
