@@ -229,7 +229,7 @@ def main():
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only: --gpus {args.gpus} is not supported "
-              "(the path shards by rollout with no exchange; see DESIGN.md)", file=sys.stderr)
+              "(the path shards by whole rollouts with no exchange between GPUs)", file=sys.stderr)
         sys.exit(2)
 
     import torch

@@ -15,7 +15,8 @@ from oracle import pipeline as OP
 from synth import workloads as W
 from tests import workload_params as WP
 
-# Tolerances (Sec. 8 of the build's scope; see the design doc for their derivation)
+# Tolerances: 2e-3 on log-probabilities and turn means, 1e-4 relative on cumulative sums (the
+# stated bounds), 4e-3 on the KL estimate, a difference of two log-probabilities
 TOL_LOGP = 2e-3     # |d logp_t|, |d logp_s|, |d turn mean|
 TOL_KL = 4e-3       # |d kl| (difference of two logps)
 TOL_CUM_REL = 1e-4  # |d C| <= TOL_CUM_REL * max(|C|, 1)
