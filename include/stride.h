@@ -113,6 +113,11 @@ size_t stride_workspace_size(const stride_layout *layout, int32_t unit);
  *                    rows (one wavefront reads the token's teacher and student rows).
  *   turn_mean        [T] double output
  *   dev_flags        device uint32 or NULL
+ *
+ * Values: -inf logits carry no mass; NaN, +inf or an all -inf row raise
+ * STRIDE_FLAG_NONFINITE and give NaN outputs for that row.  Finite logits are
+ * supported up to |x| = 2^127 (the exponent is formed as x * log2(e) in fp32);
+ * rows with larger finite values are outside the supported range.
  */
 stride_status stride_score(const stride_layout *layout, int32_t vocab, int64_t ld, int32_t dtype,
                            int32_t n_teachers, const void *const *teacher_logits,
