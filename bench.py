@@ -206,6 +206,93 @@ def bench_fused(args):
     print(json.dumps(res), flush=True)
 
 
+def bench_online(args):
+    """Latency of the online stop test (stride_stop_step): per call, a batch of active rollouts
+    appends new units (one turn mean each, or a chunk of token log-probabilities each) and the
+    carried state is updated on the device.  lambda is set below every reachable value, so every
+    rollout stays active for the whole run."""
+    import torch
+    import paper_2609_14636_amd as P
+
+    stream = torch.cuda.current_stream()
+    lines = []
+    for unit, active, per in ((P.STRIDE_UNIT_TURN, 256, 1), (P.STRIDE_UNIT_TOKEN, 64, 512)):
+        g = torch.Generator(device="cuda").manual_seed(args.seed)
+        dt = torch.float64 if unit == P.STRIDE_UNIT_TURN else torch.float32
+        vals = -torch.rand(active * per, generator=g, device="cuda", dtype=torch.float64).to(dt)
+        slot = torch.arange(active, dtype=torch.int32, device="cuda")
+        off = torch.arange(0, active * per + 1, per, dtype=torch.int64, device="cuda")
+        cum = torch.zeros(active, dtype=torch.float64, device="cuda")
+        units = torch.zeros(active, dtype=torch.int32, device="cuda")
+        stop = torch.full((active,), -1, dtype=torch.int32, device="cuda")
+        flags = torch.zeros(1, dtype=torch.int32, device="cuda")
+        lam = [-1e300]
+
+        def call():
+            P.stride_stop_step(slot, off, unit, vals, None, lam, cum, units, stop, flags)
+
+        for _ in range(args.warmup):
+            call()
+        torch.cuda.synchronize()
+        calls = max(args.steps, 1) * 10
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(calls):
+            call()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        us = e0.elapsed_time(e1) * 1e3 / calls
+        t0 = time.perf_counter()
+        for _ in range(calls):
+            call()
+            torch.cuda.synchronize()
+        rt = (time.perf_counter() - t0) * 1e6 / calls
+        if int(flags.item()) != 0 or int((stop >= 0).sum().item()) != 0:
+            raise SystemExit("online stop test: unexpected flags or stops")
+        name = "turn" if unit == P.STRIDE_UNIT_TURN else "token"
+        lines.append({
+            "metric": "online stop test latency (stride_stop_step), 1 MI355X", "value": us,
+            "unit": "us/call", "n_gpus": 1, "steps": calls, "warmup": args.warmup,
+            "ms_per_step": us * 1e-3, "higher_is_better": False, "scaling": "weak",
+            "vs_baseline": None, "dtype": "f64" if unit == P.STRIDE_UNIT_TURN else "f32",
+            "data": "synthetic",
+            "config": {"workload": f"online {name} units: {active} active rollouts x {per} new "
+                                   f"unit(s) per call", "global_batch": active, "seq_len": per,
+                       "parallelism": "single GPU"},
+            "host_round_trip_us": rt})
+    for line in lines:
+        print(json.dumps(line), flush=True)
+
+
+def bench_records(args):
+    """Host trajectory record H(x): put a record per task, then plan every task's restart point
+    in one call (Sec. 4.2 on the host)."""
+    import paper_2609_14636_amd as P
+
+    rng = np.random.default_rng(args.seed)
+    n_tasks, turns = 100_000, 12
+    vals = -np.abs(rng.normal(0.7, 0.3, size=(n_tasks, turns)))
+    mask = (rng.random((n_tasks, turns)) < 0.9).astype(np.uint8)
+    rec = P.Records()
+    t0 = time.perf_counter()
+    for t in range(n_tasks):
+        rec.put(t, vals[t], mask[t])
+    put_s = time.perf_counter() - t0
+    tasks = np.arange(n_tasks, dtype=np.int64)
+    t0 = time.perf_counter()
+    ks, k0, km = rec.plan(tasks, -0.8)
+    plan_s = time.perf_counter() - t0
+    assert len(rec) == n_tasks and (k0 >= 0).all() and (km <= turns).all()
+    print(json.dumps({
+        "metric": "trajectory record plan throughput (stride_records_plan), host", "value":
+        n_tasks / plan_s, "unit": "tasks/s", "n_gpus": 0, "steps": 1, "warmup": 0,
+        "ms_per_step": plan_s * 1e3, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "f64", "data": "synthetic",
+        "config": {"workload": f"records: {n_tasks} tasks x {turns} turns", "global_batch": n_tasks,
+                   "seq_len": turns, "parallelism": "host, one thread"},
+        "put_tasks_per_s_with_binding": n_tasks / put_s}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -222,6 +309,10 @@ def main():
                     help="also compute the exact full-vocabulary KL per token (paired kernel)")
     ap.add_argument("--opd-grad", action="store_true",
                     help="also run the OPD loss gradient (stride_opd_grad) in each step")
+    ap.add_argument("--online", action="store_true",
+                    help="only time the online stop test (stride_stop_step) per call")
+    ap.add_argument("--records", action="store_true",
+                    help="only time the host trajectory record (put / plan)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="only run a plain elementwise copy (torch.neg on float32) reading and "
                          "writing BYTES each per dispatch, to calibrate the HBM byte counters; keep "
@@ -247,11 +338,16 @@ def main():
         print(json.dumps({"copy_calibration_bytes": 4 * n, "launches": 3}), flush=True)
         return
 
+    if args.records:
+        return bench_records(args)
+
     import paper_2609_14636_amd as P
     from synth import workloads as W
     from tests import harness as H
 
     torch.cuda.set_device(0)
+    if args.online:
+        return bench_online(args)
     if args.workload == "fused":
         return bench_fused(args)
     wl = W.make(args.workload, seed=args.seed)
