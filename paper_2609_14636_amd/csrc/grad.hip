@@ -135,7 +135,7 @@ __global__ __launch_bounds__(256) void opd_grad_kernel(GradArgs a) {
     const float lse_l2 = (sy - lps) * kLog2e;
     const int64_t yv = ok ? (int64_t)(y / E) : -1;
     const int yj = ok ? y % E : 0;
-    auto grad_vec = [&](const u32x4 v, int64_t vi, int count) -> u32x4 {
+    auto grad_vec = [&](const u32x4 v, int64_t vi) -> u32x4 {
         float x[E];
         if (DT == STRIDE_BF16) {
 #pragma unroll
@@ -163,7 +163,6 @@ __global__ __launch_bounds__(256) void opd_grad_kernel(GradArgs a) {
 #pragma unroll
             for (int i = 0; i < 4; ++i) o[i] = __float_as_uint(g[i]);
         }
-        (void)count;
         return o;
     };
     constexpr int U = 4;
@@ -175,15 +174,15 @@ __global__ __launch_bounds__(256) void opd_grad_kernel(GradArgs a) {
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             const int64_t vi = k + u * kWave + lane;
-            __builtin_nontemporal_store(grad_vec(v[u], vi, E), dst + vi);
+            __builtin_nontemporal_store(grad_vec(v[u], vi), dst + vi);
         }
     }
     for (; k < nvec; k += kWave) {
         const int64_t vi = k + lane;
-        if (vi < nvec) __builtin_nontemporal_store(grad_vec(__builtin_nontemporal_load(src + vi), vi, E), dst + vi);
+        if (vi < nvec) __builtin_nontemporal_store(grad_vec(__builtin_nontemporal_load(src + vi), vi), dst + vi);
     }
     if (tail && lane == 0) {
-        const u32x4 g = grad_vec(src[nvec], nvec, tail);
+        const u32x4 g = grad_vec(src[nvec], nvec);
         for (int j = 0; j < tail; ++j) {
             if (DT == STRIDE_BF16)
                 reinterpret_cast<uint16_t *>(dst + nvec)[j] =

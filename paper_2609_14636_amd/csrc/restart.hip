@@ -9,7 +9,7 @@
 // records the generated turns).  Ties go to the lowest index.
 //
 // One workgroup per rollout.  Pass 1 finds the first non-correct unit of the
-// record with a block-wide integer min over 256-unit chunks, stopping at the
+// record with a block-wide integer min over 2048-unit chunks, stopping at the
 // first chunk that has one.  Pass 2 takes the lexicographic min of
 // (value, index) over [0, K_max), so the pick is exact and deterministic.
 #include <climits>
@@ -74,15 +74,23 @@ __global__ __launch_bounds__(256) void restart_kernel(RestartArgs a) {
     const VT *vals = static_cast<const VT *>(a.values);
 
     // ---- pass 1: K_max = first non-correct unit in [0, len), else len ----
+    // chunks of 8 units per thread (eight loads in flight); the first chunk holding a
+    // non-correct unit ends the search, and the min over it is exact
+    constexpr int PU = 8;
     if (tid == 0) s_min = len;
     __syncthreads();
-    for (int64_t c = 0; c < len; c += blockDim.x) {
-        const int64_t u = c + tid;
-        if (u < len) {
-            const double v = (double)vals[first + u];
-            const bool ok = (a.mask == nullptr || a.mask[first + u] != 0) && (v > alpha);
-            if (!ok) atomicMin((unsigned long long *)&s_min, (unsigned long long)u);
+    for (int64_t c = 0; c < len; c += (int64_t)blockDim.x * PU) {
+        int64_t local = LLONG_MAX;
+#pragma unroll
+        for (int k = 0; k < PU; ++k) {
+            const int64_t u = c + (int64_t)k * blockDim.x + tid;
+            if (u < len) {
+                const double v = (double)vals[first + u];
+                const bool ok = (a.mask == nullptr || a.mask[first + u] != 0) && (v > alpha);
+                if (!ok && u < local) local = u;
+            }
         }
+        if (local != LLONG_MAX) atomicMin((unsigned long long *)&s_min, (unsigned long long)local);
         __syncthreads();
         const bool done = s_min < len;
         __syncthreads();  // every thread has read s_min before any thread updates it again
@@ -93,11 +101,22 @@ __global__ __launch_bounds__(256) void restart_kernel(RestartArgs a) {
     // ---- pass 2: lowest index of the minimum over [0, K_max) ----
     double best = __builtin_inf();
     int64_t bidx = LLONG_MAX;
-    for (int64_t u = tid; u < kmax; u += blockDim.x) {
-        const double v = (double)vals[first + u];
-        if (v < best) {  // u increases, so the first hit per thread is its lowest index
-            best = v;
-            bidx = u;
+    for (int64_t c = 0; c < kmax; c += (int64_t)blockDim.x * PU) {
+        double v[PU];
+#pragma unroll
+        for (int k = 0; k < PU; ++k) {
+            const int64_t u = c + (int64_t)k * blockDim.x + tid;
+            v[k] = u < kmax ? (double)vals[first + u] : __builtin_inf();
+        }
+#pragma unroll
+        for (int k = 0; k < PU; ++k) {
+            const int64_t u = c + (int64_t)k * blockDim.x + tid;
+            // u increases, so the first hit per thread is its lowest index; the first unit
+            // always counts, so values of +inf still give an index
+            if (u < kmax && (v[k] < best || bidx == LLONG_MAX)) {
+                best = v[k];
+                bidx = u;
+            }
         }
     }
 #pragma unroll

@@ -5,7 +5,8 @@
 // log pi_S(y) - log pi_T(y) (= -r_t of Eq. 1), written for the same rows in the
 // same pass.
 //
-// One workgroup per turn.  Thread j sums rows a+j, a+j+256, ... in double;
+// One workgroup per turn.  Thread j sums rows a+j, a+j+256, ... in double
+// (four rows in flight at a time, added in that order);
 // the 256 partial sums are combined by a fixed shuffle tree and a fixed
 // cross-wave order, so the mean does not depend on scheduling.  The kernel
 // reads 4 (or 8) bytes per row and is latency-bound; it sits next to the
@@ -15,8 +16,10 @@
 namespace stride {
 namespace {
 
-__global__ __launch_bounds__(256) void turn_mean_kernel(stride_layout L, const float *logp_t,
-                                                        const float *logp_s, float *kl,
+__global__ __launch_bounds__(256) void turn_mean_kernel(stride_layout L,
+                                                        const float *__restrict__ logp_t,
+                                                        const float *__restrict__ logp_s,
+                                                        float *__restrict__ kl,
                                                         double *turn_mean, uint32_t *flags) {
     __shared__ double part[256 / kWave];
     const int64_t t = blockIdx.x;
@@ -30,8 +33,27 @@ __global__ __launch_bounds__(256) void turn_mean_kernel(stride_layout L, const f
         }
         return;
     }
+    // four rows per thread in flight; the additions keep the row order a+j, a+j+256, ...
     double acc = 0.0;
-    for (int64_t i = a + threadIdx.x; i < b; i += blockDim.x) {
+    constexpr int U = 4;
+    const int64_t stride = blockDim.x;
+    int64_t i = a + threadIdx.x;
+    for (; i + (U - 1) * stride < b; i += U * stride) {
+        float lt[U], ls[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) lt[u] = logp_t[i + u * stride];
+        if (kl) {
+#pragma unroll
+            for (int u = 0; u < U; ++u) ls[u] = logp_s[i + u * stride];
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) acc += (double)lt[u];
+        if (kl) {
+#pragma unroll
+            for (int u = 0; u < U; ++u) kl[i + u * stride] = ls[u] - lt[u];
+        }
+    }
+    for (; i < b; i += stride) {
         const float lt = logp_t[i];
         acc += (double)lt;
         if (kl) kl[i] = logp_s[i] - lt;

@@ -106,3 +106,37 @@ def test_fused_wide_hidden_size():
     assert d <= H.TOL_LOGP, d
     rep = H.compare(wl, gpu, ora, lam, alpha)
     say(f"[fused d=4096] max |d logp_t| {d:.2e}; {rep}")
+
+
+def test_restart_pick_with_infinite_values_and_long_records():
+    """Argmin ties at +inf go to the lowest index, as in the oracle; long token-unit records
+    (several 2048-unit chunks of the first pass) keep the exact K_max and k*."""
+    import torch
+    import paper_2609_14636_amd as P
+    g = np.random.default_rng(8)
+    sizes = np.array([3, 5000, 1, 9000])
+    off = np.zeros(sizes.size + 1, np.int64)
+    off[1:] = np.cumsum(sizes)
+    vals = -np.abs(g.normal(1.0, 0.5, size=int(off[-1])))
+    vals[off[0]:off[1]] = np.inf                      # rollout 0: all +inf
+    vals[off[1] + 4321] = -50.0                       # rollout 1: weakest unit deep in the record
+    mask = np.ones(vals.size, np.uint8)
+    mask[off[3] + 7001] = 0                           # rollout 3: K_max = 7001
+    alpha = -np.inf
+    vals = vals.astype(np.float32)                    # token units arrive as float32
+    ks_o, k0_o, km_o = H.OP.O.restart(off, vals.astype(np.float64), sizes.astype(np.int32),
+                                      np.full(sizes.size, alpha), mask)
+    rto = torch.arange(sizes.size + 1, dtype=torch.int32, device="cuda")  # one turn per rollout
+    tto = torch.from_numpy(off).cuda()
+    lay = P.Layout(rto, tto, int(off[-1]))
+    ks = torch.empty(sizes.size, dtype=torch.int32, device="cuda")
+    k0, km = torch.empty_like(ks), torch.empty_like(ks)
+    flags = torch.zeros(1, dtype=torch.int32, device="cuda")
+    P.stride_restart_turn(lay, P.STRIDE_UNIT_TOKEN, torch.from_numpy(vals).cuda(),
+                          None, [alpha], torch.from_numpy(mask).cuda(), ks, k0, km, flags)
+    torch.cuda.synchronize()
+    assert int(flags.item()) == 0
+    assert ks.cpu().tolist() == list(ks_o) and k0.cpu().tolist() == list(k0_o)
+    assert km.cpu().tolist() == list(km_o)
+    assert list(ks_o)[:2] == [0, 4321] and list(km_o)[3] == 7001
+    say(f"[restart edges] k* {ks.cpu().tolist()} K_max {km.cpu().tolist()}")
