@@ -33,10 +33,32 @@ STATUS_NAMES = {0: "STRIDE_OK", 1: "STRIDE_ERR_INVALID_ARG", 2: "STRIDE_ERR_UNSU
                 3: "STRIDE_ERR_WORKSPACE", 4: "STRIDE_ERR_HIP"}
 
 
+FLAG_NAMES = {STRIDE_FLAG_TOKEN_OOB: "TOKEN_OOB", STRIDE_FLAG_EMPTY_TURN: "EMPTY_TURN",
+              STRIDE_FLAG_BAD_OFFSETS: "BAD_OFFSETS", STRIDE_FLAG_NONFINITE: "NONFINITE",
+              STRIDE_FLAG_BAD_DOMAIN: "BAD_DOMAIN", STRIDE_FLAG_SPIN_LIMIT: "SPIN_LIMIT"}
+
+
+def flag_names(flags: int) -> list[str]:
+    """Names of the data-error bits set in a device flag word (unknown bits as hex)."""
+    names = [n for bit, n in FLAG_NAMES.items() if flags & bit]
+    rest = flags & ~sum(FLAG_NAMES)
+    if rest:
+        names.append(hex(rest))
+    return names
+
+
 class StrideError(RuntimeError):
     def __init__(self, status: int, message: str):
         super().__init__(f"{STATUS_NAMES.get(status, status)}: {message}")
         self.status = status
+
+
+class StrideDataError(RuntimeError):
+    """Raised by Path.check when the device flag word reports data errors."""
+
+    def __init__(self, flags: int):
+        super().__init__("device data errors: " + ", ".join(flag_names(flags)))
+        self.flags = flags
 
 
 class _CLayout(ctypes.Structure):
@@ -366,6 +388,13 @@ class Path:
         self.score(vocab, teachers, student, token_ids, stream)
         self.stop(lam, start_unit, stream)
         self.restart(alpha, correct_mask, stream)
+
+    def check(self) -> None:
+        """Synchronise on the flag word and raise StrideDataError if any data error was
+        flagged (bad token ids, empty turns, bad offsets or domains, non-finite rows)."""
+        f = int(self.flags.cpu().item()) & 0xFFFFFFFF
+        if f:
+            raise StrideDataError(f)
 
     def host(self) -> dict:
         out = {k: getattr(self, k) for k in ("logp_t", "logp_s", "kl", "kl_full", "turn_mean",

@@ -129,3 +129,11 @@ def test_probe_read_argument_errors(case):
         else:
             P.stride_probe_read(a, None, 64, None, stream=0)
     assert ei.value.status == (2 if case == "misaligned_stride" else 1)
+
+
+def test_flag_word_decoding():
+    assert P.flag_names(0) == []
+    assert P.flag_names(P.STRIDE_FLAG_TOKEN_OOB | P.STRIDE_FLAG_NONFINITE) == ["TOKEN_OOB", "NONFINITE"]
+    assert P.flag_names(1 << 20) == [hex(1 << 20)]
+    err = P.StrideDataError(P.STRIDE_FLAG_EMPTY_TURN | P.STRIDE_FLAG_SPIN_LIMIT)
+    assert "EMPTY_TURN" in str(err) and "SPIN_LIMIT" in str(err) and err.flags == 34

@@ -185,6 +185,8 @@ def test_data_error_flags():
     assert np.isfinite(out["logp_t"][[3, 6, 7, 8]]).all()
     assert np.isnan(out["kl"][[0, 1, 2, 4, 5]]).all()
     assert out["flags"] & P.STRIDE_FLAG_NONFINITE and out["flags"] & P.STRIDE_FLAG_TOKEN_OOB
+    with pytest.raises(P.StrideDataError, match="NONFINITE"):
+        path.check()
     assert np.isnan(out["turn_mean"][0]) and np.isfinite(out["turn_mean"][2])
     # the oracle agrees on the valid row 3 (the -inf entry only removes mass)
     row3 = wl.teacher_rows_host(3, 1)
