@@ -330,7 +330,10 @@ __global__ __launch_bounds__(256) void fused_merge_kernel(const float2 *partial,
         raise_flag(flags, bad);
         logp_t[row] = __builtin_nanf("");
     } else {
-        logp_t[row] = (z - m) - __builtin_amdgcn_logf(s) * kLn2;
+        // z_y comes from its own fp32 dot product and (m, s) from the MFMA accumulators, so
+        // their rounding differs by ~1e-6 relative; a log-probability is at most 0, and
+        // clamping there only moves a rounding excess toward the true value.
+        logp_t[row] = fminf(0.0f, (z - m) - __builtin_amdgcn_logf(s) * kLn2);
     }
 }
 

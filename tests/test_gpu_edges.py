@@ -140,3 +140,35 @@ def test_restart_pick_with_infinite_values_and_long_records():
     assert km.cpu().tolist() == list(km_o)
     assert list(ks_o)[:2] == [0, 4321] and list(km_o)[3] == 7001
     say(f"[restart edges] k* {ks.cpu().tolist()} K_max {km.cpu().tolist()}")
+
+
+def test_fused_confident_teacher_log_probability_is_at_most_zero():
+    """A hidden state aligned with the sampled token's weight row makes the teacher nearly
+    certain (p ~ 1): the fused log-probability must stay <= 0 and match the oracle."""
+    import torch
+    import paper_2609_14636_amd as P
+    wl = W.make("fused", seed=99, scale=dict(R=1, turns=1, tok=64, vocab=1000, d=128))
+    inp = H.device_inputs_fused(wl)
+    ids = inp["ids"]
+    w = inp["w"].float()
+    # h = 40 * w_y / |w_y|^2 puts z_y near 40 while the other logits stay O(1)
+    wy = w[ids.long()]
+    h = (40.0 * wy / (wy * wy).sum(1, keepdim=True)).to(torch.bfloat16)
+    N = wl.n_tokens
+    lt = torch.empty(N, dtype=torch.float32, device="cuda")
+    tm = torch.empty(wl.n_turns, dtype=torch.float64, device="cuda")
+    flags = torch.zeros(1, dtype=torch.int32, device="cuda")
+    ws = torch.empty(P.stride_fused_workspace_size(inp["layout"], wl.vocab), dtype=torch.uint8,
+                     device="cuda")
+    P.stride_score_fused(inp["layout"], wl.vocab, h, inp["w"], None, ids, lt, None, None, tm,
+                         flags, ws)
+    torch.cuda.synchronize()
+    assert int(flags.item()) == 0
+    got = lt.cpu().numpy()
+    assert np.all(got <= 0.0), got.max()
+    hb = h.cpu().view(torch.int16).numpy().view(np.uint16)
+    w_dv = np.ascontiguousarray(inp["w"].cpu().view(torch.int16).numpy().view(np.uint16).T)
+    want, _, fl = H.OP.O.fused_logp(hb, w_dv, wl.tok)
+    assert fl == 0 and np.max(want) <= 0
+    assert np.max(np.abs(got - want)) <= H.TOL_LOGP, np.max(np.abs(got - want))
+    say(f"[fused confident] logp in [{got.min():.2e}, {got.max():.2e}], max |d| {np.max(np.abs(got - want)):.2e}")
