@@ -319,6 +319,9 @@ __global__ __launch_bounds__(256) void score_pairs_kernel(PairArgs a) {
         // +inf when the teacher gives no mass where the student has some
         float kl = bad ? __builtin_nanf("") : (am / zs - (ms - mt)) - (ls - lt);
         if (!(kl == kl)) bad |= STRIDE_FLAG_NONFINITE;
+        // KL >= 0 (Gibbs); when the two rows differ by a constant the fp32 terms cancel to a
+        // rounding residue of either sign, and clamping only reduces that error (NaN stays NaN)
+        if (kl < 0.0f) kl = 0.0f;
         a.kl_full[row] = kl;
         if (y < 0 || y >= a.vocab) bad |= STRIDE_FLAG_TOKEN_OOB;
         float rt, rs;
