@@ -6,7 +6,11 @@ line with scored tokens/s, the roofline of the dominant kernel (the row
 scoring kernel, timed with HIP events on the stream it runs on) and the
 float64 CPU oracle timed on a bounded sample of the same workload.
 
-    python bench.py [--steps K] [--warmup W] [--workload agentic|reasoning|multi|tiny]
+    python bench.py [--steps K] [--warmup W] [--workload reasoning|agentic|multi|tiny|fused]
+
+The default workload is the long single-turn reasoning batch (8 rollouts x
+16,384 tokens, token units, V = 151,936 bf16): the largest of the
+logits-streaming workloads, 79.7 GB of logits per step.
 """
 from __future__ import annotations
 
@@ -34,6 +38,12 @@ SCORE_SRC = os.path.join(ROOT, "paper_2609_14636_amd", "csrc", "score.hip")
 
 def log(*a):
     print(*a, file=sys.stderr, flush=True)
+
+
+def stats_ms(pairs):
+    """mean, median and min of the elapsed times (ms) of a list of (start, end) events."""
+    t = np.array([a.elapsed_time(b) for a, b in pairs], dtype=np.float64)
+    return {"mean": float(t.mean()), "median": float(np.median(t)), "min": float(t.min())}
 
 
 def workload_params(name: str, seed: int):
@@ -77,6 +87,19 @@ def measured_traffic(workload: str, kernel_src: str = None, key: str = "score_hi
     return e["fetch_kib"] * 1024.0 * k_fetch + e["write_kib"] * 1024.0 * k_write
 
 
+def measured_mfma_busy():
+    """Matrix-core busy fraction of the fused projection kernel from committed rocprofv3
+    counters (SQ_VALU_MFMA_BUSY_CYCLES over four SIMDs per CU times GRBM_GUI_ACTIVE per XCD),
+    if they were taken on the current fused.hip; else None."""
+    if not os.path.exists(TRAFFIC):
+        return None
+    with open(TRAFFIC) as f:
+        e = json.load(f).get("fused_mfma")
+    if not e or e.get("fused_hip_sha256_16") != source_digest(FUSED_SRC):
+        return None
+    return {k: e[k] for k in ("busy_frac", "clock_GHz", "counters")}
+
+
 def cpu_baseline(wl, lam, alpha, budget_s: float):
     """Float64 oracle on whole rollouts of the workload, in order, until budget_s seconds of
     oracle compute (at least one rollout); compute time only, host input generation excluded."""
@@ -114,7 +137,7 @@ def cpu_baseline_fused(wl, budget_s: float):
     from tests import harness as H
 
     threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
-    w_dv = np.ascontiguousarray(wl.w_host(threads).T)
+    w_dv = wl.w_dv_host(threads)
     rows, t_ora, r0 = 0, 0.0, 0
     while rows == 0 or (t_ora < budget_s and r0 < wl.n_tokens):
         idx = np.arange(r0, min(r0 + 16, wl.n_tokens))
@@ -130,6 +153,69 @@ def cpu_baseline_fused(wl, budget_s: float):
             "sample": f"rows 0..{rows - 1} of the timed workload (teacher logits h W formed in "
                       f"binary64 over d={wl.fused_d}, V={wl.vocab}, plus the student row); "
                       f"oracle compute {t_ora:.1f} s"}
+
+
+def retained_row_mask(wl, stop, start):
+    """1 for the rows the OPD loss keeps (units K0 .. stop of each rollout, to its last unit
+    without a stop), 0 elsewhere, on the host from the stop indices (a measurement aid)."""
+    from synth import workloads as W
+    m = np.zeros(wl.n_tokens, np.uint8)
+    for r in range(wl.n_rollouts):
+        t0, t1 = int(wl.rollout_turn_off[r]), int(wl.rollout_turn_off[r + 1])
+        a = int(wl.turn_tok_off[t0])
+        n = (t1 - t0) if wl.unit == W.UNIT_TURN else int(wl.turn_tok_off[t1]) - a
+        k0 = 0 if start is None else int(min(max(int(start[r]), 0), n))
+        last = int(stop[r]) if 0 <= int(stop[r]) < n else n - 1
+        if last < k0:
+            continue
+        if wl.unit == W.UNIT_TURN:
+            m[int(wl.turn_tok_off[t0 + k0]):int(wl.turn_tok_off[t0 + last + 1])] = 1
+        else:
+            m[a + k0:a + last + 1] = 1
+    return m
+
+
+def bench_read_sweep(args):
+    """Read rate against footprint on the buffers of a logits workload: the first n rows of the
+    teacher and student matrices, read with the scoring kernel's pattern (stride_probe_read) and
+    as two contiguous ranges in grid-stride order (stride_probe_read_flat)."""
+    import torch
+
+    import paper_2609_14636_amd as P
+    from synth import workloads as W
+    from tests import harness as H
+
+    wl = W.make(args.workload, seed=args.seed)
+    inp = H.device_inputs(wl)
+    t, st = inp["teachers"][0], inp["student"]
+    N = wl.n_tokens
+    row_bytes = t.stride(0) * t.element_size()
+    stream = torch.cuda.current_stream()
+    sink = torch.empty(2 * N, dtype=torch.int32, device="cuda")
+    torch.cuda.synchronize()
+    reps = max(args.steps // 2, 3)
+    for frac in (1 / 6, 1 / 3, 1 / 2, 2 / 3, 5 / 6, 1.0):
+        n = int(N * frac)
+        nbytes = 2 * n * row_bytes
+        out = {"metric": "streaming read rate against footprint", "unit": "GB/s",
+               "workload": args.workload, "rows_per_matrix": n, "footprint_GB": nbytes / 1e9}
+        for name, call in (
+                ("rows", lambda: P.stride_probe_read(t[:n], st[:n], row_bytes, sink)),
+                ("flat", lambda: P.stride_probe_read_flat(t[:n], st[:n], n * row_bytes, sink))):
+            call()
+            ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+                  for _ in range(reps)]
+            for a, b in ev:
+                a.record(stream)
+                call()
+                b.record(stream)
+            torch.cuda.synchronize()
+            tm = stats_ms(ev)
+            out[name] = {"ms_median": tm["median"], "GBs_median": nbytes / (tm["median"] * 1e-3) / 1e9,
+                         "GBs_best": nbytes / (tm["min"] * 1e-3) / 1e9}
+        log(f"[sweep] {nbytes / 1e9:.1f} GB: rows {out['rows']['GBs_median']:.0f} GB/s, "
+            f"flat {out['flat']['GBs_median']:.0f} GB/s")
+        print(json.dumps(out), flush=True)
 
 
 def bench_fused(args):
@@ -177,7 +263,8 @@ def bench_fused(args):
                              lt, None, None, tm, path.flags, path.fused_ws)
         b.record(stream)
     torch.cuda.synchronize()
-    k_ms = sum(a.elapsed_time(b) for a, b in ev) / len(ev)
+    k_stats = stats_ms(ev)
+    k_ms = k_stats["mean"]
     flops = 2.0 * wl.n_tokens * wl.fused_d * wl.vocab
     achieved = flops / (k_ms * 1e-3) / 1e12
     log(f"[bench] {args.steps} steps: {ms_step:.3f} ms/step; teacher projection {k_ms:.3f} ms "
@@ -197,7 +284,9 @@ def bench_fused(args):
                      "traffic": measured_traffic("fused", FUSED_SRC, "fused_hip_sha256_16"),
                      "kernel": "fused_lse_kernel (bf16 MFMA 32x32x16); kernel_ms brackets the "
                                "teacher call (projection + per-row gather + merge)",
-                     "kernel_ms": k_ms,
+                     "kernel_ms": k_ms, "kernel_ms_median": k_stats["median"],
+                     "kernel_ms_min": k_stats["min"],
+                     "mfma_busy": measured_mfma_busy(),
                      "flops_per_launch": flops},
     }
     if not args.no_cpu:
@@ -298,7 +387,7 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", default="agentic",
+    ap.add_argument("--workload", default="reasoning",
                     choices=["tiny", "agentic", "reasoning", "multi", "fused"])
     ap.add_argument("--seed", type=int, default=1001)
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
@@ -313,6 +402,9 @@ def main():
                     help="only time the online stop test (stride_stop_step) per call")
     ap.add_argument("--records", action="store_true",
                     help="only time the host trajectory record (put / plan)")
+    ap.add_argument("--read-sweep", action="store_true",
+                    help="only measure the streaming read rate against footprint on the "
+                         "workload's logits buffers (row pattern and grid-stride order)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="only run a plain elementwise copy (torch.neg on float32) reading and "
                          "writing BYTES each per dispatch, to calibrate the HBM byte counters; keep "
@@ -348,6 +440,8 @@ def main():
     torch.cuda.set_device(0)
     if args.online:
         return bench_online(args)
+    if args.read_sweep:
+        return bench_read_sweep(args)
     if args.workload == "fused":
         return bench_fused(args)
     wl = W.make(args.workload, seed=args.seed)
@@ -382,6 +476,7 @@ def main():
 
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
           for _ in range(args.steps)]
+    sev = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     gev.clear()
@@ -391,6 +486,7 @@ def main():
         ev[i][1].record(stream)
         path.stop(lam, inp["start"])
         path.restart(alpha, inp["mask"])
+        sev[i].record(stream)
         if args.opd_grad:
             e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
             e0.record(stream)
@@ -401,12 +497,16 @@ def main():
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     ms_step = (t1 - t0) * 1e3 / args.steps
-    score_ms = sum(a.elapsed_time(b) for a, b in ev) / args.steps
+    k_stats = stats_ms(ev)
+    step_stats = stats_ms([(ev[i][0], sev[i]) for i in range(args.steps)])
+    score_ms = k_stats["mean"]
     out = path.host()
     if out["flags"] != 0:
         raise SystemExit(f"device flags {out['flags']:#x} on the benchmark workload")
     H.assert_invariants(out, wl)
-    log(f"[bench] {args.steps} steps: {ms_step:.3f} ms/step, scoring {score_ms:.3f} ms; "
+    log(f"[bench] {args.steps} steps: {ms_step:.3f} ms/step (device: median "
+        f"{step_stats['median']:.3f}, min {step_stats['min']:.3f}), scoring mean {score_ms:.3f} "
+        f"median {k_stats['median']:.3f} min {k_stats['min']:.3f} ms; "
         f"stops {int((out['stop_unit'] >= 0).sum())}/{wl.n_rollouts}")
 
     n_tok = wl.n_tokens
@@ -438,6 +538,7 @@ def main():
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": ms_step,
+        "step_ms": step_stats,
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -451,21 +552,44 @@ def main():
                      "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
                      "kernel": (f"score_pairs_kernel<{dt}> (with exact KL)" if args.exact_kl
                                 else f"score_rows_kernel<{dt}>"), "kernel_ms": score_ms,
+                     "kernel_ms_median": k_stats["median"], "kernel_ms_min": k_stats["min"],
                      "bytes_per_launch": bytes_alg,
                      "read_ceiling": {"achieved": ceiling, "unit": "GB/s", "frac": achieved / ceiling,
                                       "kernel": "probe_read_kernel: the same rows, same loads, "
                                                 "no arithmetic"}},
     }
     if args.opd_grad:
-        g_ms = sum(a.elapsed_time(b) for a, b in gev) / len(gev)
-        uoff = wl.unit_off()
+        g = stats_ms(gev)
+        g_ms = g["mean"]
         kept = int(out["retained"].sum())
         gbytes = kept * 2 * wl.vocab * wl.esize + (n_tok - kept) * wl.vocab * wl.esize + 13 * n_tok
-        res["opd_grad"] = {"kernel_ms": g_ms, "retained_rows": kept,
+        # read+write reference on the same rows: retained rows copied from the student logits,
+        # the others zero-filled without a read, one wavefront per row (the gradient's pattern)
+        rmask = torch.from_numpy(retained_row_mask(wl, out["stop_unit"], wl.start)).cuda()
+        assert int(rmask.sum().item()) == kept
+        row_bytes = (wl.vocab * wl.esize) // 16 * 16
+        cev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+               for _ in range(max(args.steps // 2, 3))]
+        P.stride_probe_copy(inp["student"], grad, rmask, row_bytes)
+        for a, b in cev:
+            a.record(stream)
+            P.stride_probe_copy(inp["student"], grad, rmask, row_bytes)
+            b.record(stream)
+        torch.cuda.synchronize()
+        c_ms = stats_ms(cev)["mean"]
+        cbytes = kept * 2 * row_bytes + (n_tok - kept) * row_bytes
+        copy_gbs = cbytes / (c_ms * 1e-3) / 1e9
+        res["opd_grad"] = {"kernel_ms": g_ms, "kernel_ms_median": g["median"],
+                           "kernel_ms_min": g["min"], "retained_rows": kept,
                            "bytes_per_launch": gbytes, "achieved_GBs": gbytes / (g_ms * 1e-3) / 1e9,
-                           "frac": gbytes / (g_ms * 1e-3) / 1e9 / HBM_PEAK_GBS}
+                           "frac": gbytes / (g_ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
+                           "copy_ceiling": {"achieved_GBs": copy_gbs, "kernel_ms": c_ms,
+                                            "frac": gbytes / (g_ms * 1e-3) / 1e9 / copy_gbs,
+                                            "kernel": "probe_copy_kernel: the same rows moved with "
+                                                      "the same loads and stores, no arithmetic"}}
         log(f"[bench] OPD gradient {g_ms:.3f} ms, {kept}/{n_tok} rows retained, "
-            f"{res['opd_grad']['achieved_GBs']:.0f} GB/s")
+            f"{res['opd_grad']['achieved_GBs']:.0f} GB/s; read+write reference {c_ms:.3f} ms = "
+            f"{copy_gbs:.0f} GB/s")
     if not args.no_cpu:
         log("[bench] timing the float64 oracle on a bounded sample")
         res["cpu_baseline"] = cpu_baseline(wl, lam, alpha, args.cpu_seconds)

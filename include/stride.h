@@ -64,7 +64,7 @@ enum {
     STRIDE_FLAG_EMPTY_TURN = 2,  /* a turn with no rows: its mean is NaN                            */
     STRIDE_FLAG_BAD_OFFSETS = 4, /* offsets not monotone, not starting at 0 or not ending at N/T    */
     STRIDE_FLAG_NONFINITE = 8,   /* a row holds NaN or +inf, or only -inf: its outputs are NaN      */
-    STRIDE_FLAG_BAD_DOMAIN = 16, /* domain[r] outside [0, n_teachers) or [0, n_dom)                 */
+    STRIDE_FLAG_BAD_DOMAIN = 16, /* domain[r] outside [0, n_dom), or [0, n_teachers) when routing  */
     STRIDE_FLAG_SPIN_LIMIT = 32  /* a cross-workgroup wait gave up; the scan results are not valid  */
 };
 
@@ -81,9 +81,10 @@ typedef struct {
 
 /*
  * Bytes of workspace the calls below need for this layout and unit (the
- * maximum over stride_score, stride_score_fused, stride_stop and
- * stride_restart_turn, so one buffer serves them all).  Host-only; reads only
- * the sizes in *layout.  Returns 0 for a NULL layout.
+ * maximum over stride_score, stride_stop, stride_restart_turn and
+ * stride_opd_grad, so one buffer serves them all; stride_score_fused sizes its
+ * own with stride_fused_workspace_size).  Host-only; reads only the sizes in
+ * *layout.  Returns 0 for a NULL layout.
  */
 size_t stride_workspace_size(const stride_layout *layout, int32_t unit);
 
@@ -100,11 +101,17 @@ size_t stride_workspace_size(const stride_layout *layout, int32_t unit);
  *   dtype            STRIDE_BF16 or STRIDE_F32
  *   n_teachers       1 .. STRIDE_MAX_DOMAINS
  *   teacher_logits   (host) array of n_teachers device pointers, each [N, ld];
- *                    the rows of rollout r are read from teacher domain[r]
- *                    (rows of rollouts routed elsewhere are never read)
- *   student_logits   [N, ld] or NULL (then logp_s and kl must be NULL)
+ *                    with n_teachers > 1 the rows of rollout r are read from
+ *                    teacher domain[r] (rows of rollouts routed elsewhere are
+ *                    never read) and a domain id outside [0, n_teachers) raises
+ *                    STRIDE_FLAG_BAD_DOMAIN with NaN outputs for its rows; with
+ *                    n_teachers = 1 every row reads teacher 0 and the domain ids
+ *                    are not used here (they select lambda and alpha in
+ *                    stride_stop and stride_restart_turn, which check them)
+ *   student_logits   [N, ld] or NULL (then logp_s, kl and kl_full must be NULL)
  *   token_ids        [N] int32, the sampled tokens
- *   logp_t, logp_s   [N] float outputs (logp_s may be NULL)
+ *   logp_t, logp_s   [N] float outputs; logp_s is required with student_logits
+ *                    (STRIDE_ERR_INVALID_ARG otherwise) and must be NULL without
  *   kl               [N] float output log pi_S - log pi_T, or NULL
  *   kl_full          [N] float output or NULL: the exact reverse KL over the whole
  *                    vocabulary, KL(pi_S || pi_T) = sum_v pi_S(v) log(pi_S(v) / pi_T(v)),
@@ -137,7 +144,8 @@ stride_status stride_score(const stride_layout *layout, int32_t vocab, int64_t l
  *   hidden_t         [N, d] bf16 row-major, 16-byte aligned
  *   w_t              [vocab, d] bf16 row-major (a linear layer's weight: row v
  *                    holds the weights of vocabulary entry v), 16-byte aligned
- *   student_logits   [N, ld] bf16 or NULL (as in stride_score)
+ *   student_logits   [N, ld] bf16 or NULL; logp_s is required with it and kl
+ *                    needs it (as in stride_score)
  *   ws               at least stride_fused_workspace_size(layout, vocab) bytes
  */
 stride_status stride_score_fused(const stride_layout *layout, int32_t vocab, int32_t d,
@@ -291,6 +299,43 @@ stride_status stride_records_plan(stride_records *rec, int32_t n_tasks, const in
  * STRIDE_ERR_UNSUPPORTED for misaligned rows. */
 stride_status stride_probe_read(const void *a, const void *b, int64_t n_rows, int64_t row_bytes,
                                 int64_t read_bytes, uint32_t *sink, hipStream_t stream);
+
+/* Streaming-read reference in the plainest order (a measurement aid, not a step of
+ * the method): reads the first n_bytes of a, then of b (when not NULL), as one
+ * contiguous range each, in a grid-stride order with 16-byte non-temporal loads,
+ * so that its rate, next to stride_probe_read's on the same bytes, separates the
+ * effect of the row-per-wavefront pattern from that of the footprint.
+ *   n_bytes     a multiple of 16 (>= 0); a, b 16-byte aligned
+ *   sink        [sink_len >= 4] uint32; min(2048, sink_len / 4) workgroups write
+ *               one XOR word per wavefront
+ * Errors: STRIDE_ERR_INVALID_ARG for NULL pointers or sizes out of range,
+ * STRIDE_ERR_UNSUPPORTED for misaligned ranges. */
+stride_status stride_probe_read_flat(const void *a, const void *b, int64_t n_bytes, uint32_t *sink,
+                                     int64_t sink_len, hipStream_t stream);
+
+/* Streaming read+write reference for the OPD gradient's roofline (a measurement aid,
+ * not a step of the method): moves n_rows rows as stride_opd_grad does -- one
+ * wavefront per row, a 16-byte non-temporal load and store per word -- copying the
+ * first copy_bytes of each row of src to dst; a row whose row_mask byte is 0 is
+ * written as zeros without being read (row_mask may be NULL: every row copied).
+ *   src, dst    device rows of row_bytes (a multiple of 16), 16-byte aligned
+ *   copy_bytes  in [16, row_bytes], rounded down to a multiple of 16
+ * Errors as stride_probe_read. */
+stride_status stride_probe_copy(const void *src, void *dst, const uint8_t *row_mask, int64_t n_rows,
+                                int64_t row_bytes, int64_t copy_bytes, hipStream_t stream);
+
+/* Test hook of the stop test's cross-workgroup look-back (not a step of the method).
+ *
+ * In the library built for testing (libstride_debug.so, scan compiled with
+ * STRIDE_SCAN_DELAY_HOOK), later stride_stop calls make the scan tiles
+ * picked by a hash of (seed, tile) -- about one in `one_in` -- sleep 1 .. `sleeps` times
+ * s_sleep(127) (about 8,000 cycles each) before publishing their aggregate, so that their
+ * successors look back over descriptors that are not yet published.  The waits stay far below
+ * the look-back spin limit, so every wave exits normally and the results must equal the
+ * undelayed ones bit for bit.  one_in = 0 switches the delays off.  Process-wide setting.
+ * Returns STRIDE_ERR_INVALID_ARG for sleeps outside 1 .. 1000 (with one_in > 0), and
+ * STRIDE_ERR_UNSUPPORTED in the product library (libstride.so), which has no delay code. */
+stride_status stride_debug_scan_delay(uint64_t seed, uint32_t one_in, uint32_t sleeps);
 
 /* Message for the last non-OK status returned on this thread ("" if none). */
 const char *stride_last_error(void);

@@ -165,7 +165,8 @@ int oracle_turn_mean(int64_t n_turns, const int64_t *turn_tok_off, const double 
 
 /*
  * Early-stop test, Eq. (5) (Sec. 4.1) with the prefix-buffer offset of
- * Sec. 4.1 ("Synergy with the prefix buffer") and Algorithm 1's inner loop.
+ * Sec. 4.1 (its paragraph on combining the stop with the prefix buffer) and
+ * Algorithm 1's inner loop.
  *
  * Rollout r owns units [unit_off[r], unit_off[r+1]); a unit is a turn (value =
  * lbar_k, the paper's rule) or a token (value = teacher log-prob, the
@@ -209,8 +210,8 @@ void oracle_stop(int64_t n_roll, const int64_t *unit_off, const double *values,
  * were generated: up to and including a stop, Algorithm 1), or all units if
  * record_len is NULL.  Unit u is correct iff mask[u] != 0 (mask NULL: all
  * set) and value_u > alpha[r] (strict; step 1).  K_max is the length of the
- * leading run of correct units (step 2's "longest continuous correct
- * prefix").  k* is the lowest index u < K_max attaining min value_u (Eq. 6,
+ * leading run of correct units, counted from unit 0 up to the first unit
+ * that is not correct (step 2).  k* is the lowest index u < K_max attaining min value_u (Eq. 6,
  * 0-based), -1 if K_max = 0.  K0 = max(k*, 0): the next rollout reuses
  * units 0..k*-1 as context and resamples from k* (step 3), and a task without
  * a usable prefix starts from 0.  k_max may be NULL.

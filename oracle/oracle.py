@@ -188,6 +188,36 @@ def fused_logp(hidden: np.ndarray, w: np.ndarray, ids: np.ndarray):
     return logp, lse, int(flags)
 
 
+def _bf16_bits_to_f64(bits: np.ndarray) -> np.ndarray:
+    """Exact decode of bf16 bit patterns (each is the top half of a binary32), in float64."""
+    return (bits.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+
+
+def fused_logp_matmul(hidden: np.ndarray, w: np.ndarray, ids: np.ndarray, rows_per_call: int = 256):
+    """Teacher log-probabilities of z = h W (Eq. 1 with projected logits) with the projection
+    done by a library matmul: both bf16 operands are decoded exactly to float64, z is one
+    float64 matrix product per block of rows (rows are independent), and each row of z goes
+    through logp_rows, the oracle's row log-softmax.  The same definition as fused_logp, for
+    row counts where fused_logp's plain loops are too slow; ``w`` is [d, vocab] (a transposed
+    view of a [vocab, d] array is taken as is, without copying).  Returns (logp, lse, flags)."""
+    hidden = np.ascontiguousarray(hidden, dtype=np.uint16)
+    n, d = hidden.shape
+    d2, vocab = w.shape
+    if d2 != d or w.dtype != np.uint16:
+        raise ValueError("hidden is [n, d] and w is [d, vocab], both bf16 bit patterns")
+    ids = np.ascontiguousarray(ids, dtype=np.int32)
+    w64 = _bf16_bits_to_f64(w)
+    logp = np.empty(n, np.float64)
+    lse = np.empty(n, np.float64)
+    flags = 0
+    for i in range(0, n, rows_per_call):
+        j = min(n, i + rows_per_call)
+        z = _bf16_bits_to_f64(hidden[i:j]) @ w64
+        logp[i:j], lse[i:j], f = logp_rows(z, ids[i:j])
+        flags |= f
+    return logp, lse, flags
+
+
 def opd_grad(student: np.ndarray, ids: np.ndarray, r: np.ndarray, mask: np.ndarray, scale: float,
              vocab: int | None = None):
     """Token-level OPD loss and gradient w.r.t. the student logits (Eq. 2).

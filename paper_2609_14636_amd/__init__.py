@@ -9,5 +9,7 @@ from .stride import (  # noqa: F401
     STRIDE_MAX_DOMAINS, STRIDE_UNIT_TOKEN, STRIDE_UNIT_TURN, Layout, Path, Records, StrideDataError,
     StrideError, flag_names,
     library,
-    stride_fused_workspace_size, stride_opd_grad, stride_probe_read, stride_restart_turn,
-    stride_score, stride_score_fused, stride_stop, stride_stop_step, stride_workspace_size)
+    stride_fused_workspace_size, stride_opd_grad, stride_probe_copy, stride_probe_read,
+    stride_probe_read_flat, stride_restart_turn,
+    stride_score, stride_score_fused, stride_stop, stride_stop_step,
+    stride_workspace_size)

@@ -2,7 +2,9 @@
 
 Each source is compiled by hipcc in parallel, then linked into
 ``paper_2609_14636_amd/libstride.so``.  Packed-FP32 instruction selection is
-switched off for all device code.
+switched off for all device code.  A second library for testing,
+``libstride_debug.so``, links the same objects except that the stop test's scan
+is compiled with its look-back delay hook (STRIDE_SCAN_DELAY_HOOK).
 """
 import os
 import subprocess
@@ -13,6 +15,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 PKG = os.path.dirname(HERE)
 ROOT = os.path.dirname(PKG)
 LIB = os.path.join(PKG, "libstride.so")
+DEBUG_LIB = os.path.join(PKG, "libstride_debug.so")
 BUILD = os.path.join(ROOT, "_build")
 
 SOURCES = ["stride_abi.cpp", "record.cpp", "score.hip", "turn.hip", "scan.hip", "restart.hip", "fused.hip", "grad.hip", "probe.hip"]
@@ -21,10 +24,11 @@ FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-Wall",
          "-I", os.path.join(ROOT, "include")]
 
 
-def _compile(src: str, verbose: bool) -> str:
-    obj = os.path.join(BUILD, os.path.splitext(src)[0] + ".o")
+def _compile(src: str, verbose: bool, defines=(), suffix: str = "") -> str:
+    obj = os.path.join(BUILD, os.path.splitext(src)[0] + suffix + ".o")
     lang = ["-x", "hip"] if src.endswith(".cpp") else []
-    cmd = ["hipcc", *FLAGS, *lang, "-c", os.path.join(HERE, src), "-o", obj]
+    cmd = ["hipcc", *FLAGS, *[f"-D{d}" for d in defines], *lang, "-c", os.path.join(HERE, src),
+           "-o", obj]
     if verbose:
         print(" ".join(cmd), flush=True)
     r = subprocess.run(cmd, capture_output=True, text=True)
@@ -36,18 +40,26 @@ def _compile(src: str, verbose: bool) -> str:
     return obj
 
 
-def build(verbose: bool = False) -> str:
-    os.makedirs(BUILD, exist_ok=True)
-    with ThreadPoolExecutor(min(8, len(SOURCES))) as ex:
-        objs = list(ex.map(lambda s: _compile(s, verbose), SOURCES))
-    tmp = LIB + ".tmp"
+def _link(objs, out: str, verbose: bool) -> None:
+    tmp = out + ".tmp"
     cmd = ["hipcc", "--offload-arch=gfx950", "-shared", "-fPIC", "-o", tmp, *objs]
     if verbose:
         print(" ".join(cmd), flush=True)
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"link failed:\n{r.stdout}{r.stderr}")
-    os.replace(tmp, LIB)
+    os.replace(tmp, out)
+
+
+def build(verbose: bool = False) -> str:
+    os.makedirs(BUILD, exist_ok=True)
+    jobs = [(s, (), "") for s in SOURCES] + [("scan.hip", ("STRIDE_SCAN_DELAY_HOOK",), "_debug")]
+    with ThreadPoolExecutor(min(8, len(jobs))) as ex:
+        objs = list(ex.map(lambda j: _compile(j[0], verbose, j[1], j[2]), jobs))
+    product, debug_scan = objs[:len(SOURCES)], objs[-1]
+    _link(product, LIB, verbose)
+    _link([debug_scan if SOURCES[i] == "scan.hip" else o for i, o in enumerate(product)],
+          DEBUG_LIB, verbose)
     return LIB
 
 

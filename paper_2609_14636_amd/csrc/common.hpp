@@ -29,12 +29,19 @@ struct alignas(16) TileDesc {
 // Workspace layout (byte offsets from ws, each region 256-byte aligned).
 struct WsLayout {
     size_t counter;   // uint32 tile counter + spare words
-    size_t row_dom;   // uint8 [N] teacher index per row (multi-teacher scoring)
     size_t unit_off;  // int64 [R+1] first unit of each rollout
     size_t desc;      // TileDesc [tiles]
+    size_t stop_end;  // end of the regions the stop test uses
+    size_t row_dom;   // uint8 [N] teacher index per row (multi-teacher scoring) or
+                      // retained-row mask (gradient)
     size_t fused;     // float2 [N, vocab tiles] partial (max, sum) of the fused projection
     size_t total;
 };
+
+// Largest delay the scan's test hook may add before a tile publishes: this many
+// s_sleep(127) (about 8,000 cycles each), about 4 ms, far below the look-back spin limit of
+// 4 million waits of at least 64 cycles each.
+constexpr uint32_t kMaxDelaySleeps = 1000;
 
 constexpr int kScanThreads = 256;
 constexpr int kScanItems = 8;
@@ -93,9 +100,15 @@ hipError_t launch_stop_step(int32_t n_active, const int32_t *rid, const int64_t 
                             int32_t *state_units, int32_t *stop_unit, uint32_t *flags,
                             hipStream_t stream);
 
-// restart.hip
+// probe.hip
+hipError_t launch_probe_flat(const void *a, const void *b, int64_t n_bytes, uint32_t *sink,
+                             int64_t sink_len, hipStream_t stream);
+hipError_t launch_probe_copy(const void *src, void *dst, const uint8_t *mask, int64_t n_rows,
+                             int64_t row_bytes, int64_t copy_bytes, hipStream_t stream);
 hipError_t launch_probe_read(const void *a, const void *b, int64_t n_rows, int64_t row_bytes,
                              int64_t read_bytes, uint32_t *sink, hipStream_t stream);
+
+// restart.hip
 hipError_t launch_restart(const stride_layout &L, int32_t unit, const void *values,
                           const int32_t *stop_unit, const DomainTable &alpha, int32_t n_dom,
                           const uint8_t *mask, int32_t *k_star, int32_t *k0, int32_t *k_max,

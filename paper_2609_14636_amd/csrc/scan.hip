@@ -24,6 +24,7 @@
 //      then with one global atomicMin per rollout per tile.
 // Waits are bounded: past the spin limit the tile gives up, raises
 // STRIDE_FLAG_SPIN_LIMIT and writes NaN, so no wave can hang.
+#include <atomic>
 #include <climits>
 
 #include "common.hpp"
@@ -50,7 +51,19 @@ struct StopArgs {
     uint32_t *counter;
     TileDesc *desc;
     uint32_t *flags;
+    // Test hook (the library built with STRIDE_SCAN_DELAY_HOOK only): tiles picked by a
+    // seeded hash sleep a bounded time before publishing their aggregate, so successors
+    // must wait on unpublished descriptors.  Zero in the product build.
+    uint64_t delay_seed;
+    uint32_t delay_one_in;
+    uint32_t delay_sleeps;
 };
+
+#ifdef STRIDE_SCAN_DELAY_HOOK
+std::atomic<uint64_t> g_delay_seed{0};
+std::atomic<uint32_t> g_delay_one_in{0};
+std::atomic<uint32_t> g_delay_sleeps{0};
+#endif
 
 // unit_off, stop_unit sentinels, descriptor reset, tile counter reset.
 __global__ __launch_bounds__(256) void stop_prep_kernel(StopArgs a, int64_t *unit_off) {
@@ -168,6 +181,20 @@ __global__ __launch_bounds__(kScanThreads) void stop_scan_kernel(StopArgs a) {
     if (tid == 0) {
         Seg total{0u, 0.0};
         for (int w = 0; w < kScanThreads / kWave; ++w) total = combine(total, s_wave[w]);
+#ifdef STRIDE_SCAN_DELAY_HOOK
+        if (a.delay_one_in) {
+            // splitmix64 step (Steele, Lea and Flood 2014) of (seed, tile): picks the tile
+            // and its sleep count
+            uint64_t z = a.delay_seed + 0x9E3779B97F4A7C15ull * (uint64_t)(tile + 1);
+            z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+            z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+            z ^= z >> 31;
+            if ((z % a.delay_one_in) == 0) {
+                const uint32_t n = 1 + (uint32_t)((z >> 32) % a.delay_sleeps);
+                for (uint32_t i = 0; i < n; ++i) __builtin_amdgcn_s_sleep(127);
+            }
+        }
+#endif
         a.desc[tile].value = total.v;
         a.desc[tile].head = total.f;
         __hip_atomic_store(&a.desc[tile].status, 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
@@ -362,7 +389,7 @@ hipError_t launch_stop(const stride_layout &L, int32_t unit, const void *values,
                        double *cum, int32_t *stop_unit, int64_t *retained, uint32_t *flags,
                        void *ws, hipStream_t stream) {
     const int64_t n_units = (unit == STRIDE_UNIT_TURN) ? L.n_turns : L.n_tokens;
-    const WsLayout w = ws_layout(L.n_rollouts, L.n_tokens, n_units, 0);
+    const WsLayout w = ws_layout(L.n_rollouts, 0, n_units, 0);
     char *base = static_cast<char *>(ws);
     StopArgs a;
     a.L = L;
@@ -380,6 +407,15 @@ hipError_t launch_stop(const stride_layout &L, int32_t unit, const void *values,
     a.counter = reinterpret_cast<uint32_t *>(base + w.counter);
     a.desc = reinterpret_cast<TileDesc *>(base + w.desc);
     a.flags = flags;
+#ifdef STRIDE_SCAN_DELAY_HOOK
+    a.delay_seed = g_delay_seed.load();
+    a.delay_one_in = g_delay_one_in.load();
+    a.delay_sleeps = g_delay_sleeps.load();
+#else
+    a.delay_seed = 0;
+    a.delay_one_in = 0;
+    a.delay_sleeps = 0;
+#endif
 
     const int64_t prep_n = (L.n_rollouts + 1 > a.n_tiles) ? L.n_rollouts + 1 : a.n_tiles;
     hipLaunchKernelGGL(stop_prep_kernel, dim3((unsigned)((prep_n + 255) / 256)), dim3(256), 0,
@@ -405,3 +441,18 @@ hipError_t launch_stop(const stride_layout &L, int32_t unit, const void *values,
 }
 
 }  // namespace stride
+
+extern "C" stride_status stride_debug_scan_delay(uint64_t seed, uint32_t one_in, uint32_t sleeps) {
+#ifdef STRIDE_SCAN_DELAY_HOOK
+    if (one_in > 0 && (sleeps < 1 || sleeps > stride::kMaxDelaySleeps)) return STRIDE_ERR_INVALID_ARG;
+    stride::g_delay_seed.store(seed);
+    stride::g_delay_sleeps.store(sleeps);
+    stride::g_delay_one_in.store(one_in);
+    return STRIDE_OK;
+#else
+    (void)seed;
+    (void)one_in;
+    (void)sleeps;
+    return STRIDE_ERR_UNSUPPORTED;
+#endif
+}

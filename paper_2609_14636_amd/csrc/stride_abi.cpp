@@ -18,13 +18,14 @@ WsLayout ws_layout(int64_t n_rollouts, int64_t n_tokens, int64_t n_units, int64_
     size_t off = 0;
     w.counter = off;
     off += 256;
-    w.row_dom = off;
-    off += align256((size_t)(n_tokens > 0 ? n_tokens : 0));
     w.unit_off = off;
     off += align256(sizeof(int64_t) * (size_t)(n_rollouts + 1));
     w.desc = off;
     const int64_t tiles = n_units > 0 ? (n_units + kScanTile - 1) / kScanTile : 0;
     off += align256(sizeof(TileDesc) * (size_t)tiles);
+    w.stop_end = off;
+    w.row_dom = off;
+    off += align256((size_t)(n_tokens > 0 ? n_tokens : 0));
     w.fused = off;
     off += align256(8 * (size_t)(fused_partials > 0 ? fused_partials : 0));
     w.total = off;
@@ -68,13 +69,20 @@ stride_status check_layout(const stride_layout *L) {
     return STRIDE_OK;
 }
 
-stride_status check_ws(const stride_layout *L, int64_t n_units, void *ws, size_t ws_bytes) {
-    const WsLayout w = ws_layout(L->n_rollouts, L->n_tokens, n_units, 0);
-    if (!ws) return fail(STRIDE_ERR_WORKSPACE, "workspace is NULL (need %zu bytes)", w.total);
+stride_status check_ws(size_t need, void *ws, size_t ws_bytes) {
+    if (!ws) return fail(STRIDE_ERR_WORKSPACE, "workspace is NULL (need %zu bytes)", need);
     if (!aligned(ws, 256)) return fail(STRIDE_ERR_WORKSPACE, "workspace is not 256-byte aligned");
-    if (ws_bytes < w.total)
-        return fail(STRIDE_ERR_WORKSPACE, "workspace has %zu bytes, need %zu", ws_bytes, w.total);
+    if (ws_bytes < need)
+        return fail(STRIDE_ERR_WORKSPACE, "workspace has %zu bytes, need %zu", ws_bytes, need);
     return STRIDE_OK;
+}
+
+// Bytes of workspace the row-domain table (scoring) or retained-row mask (gradient) needs.
+size_t rows_ws_bytes(const stride_layout &L) { return ws_layout(L.n_rollouts, L.n_tokens, 0, 0).total; }
+
+// Bytes of workspace the stop test needs: tile counter, unit offsets, tile descriptors.
+size_t stop_ws_bytes(const stride_layout &L, int64_t n_units) {
+    return ws_layout(L.n_rollouts, 0, n_units, 0).stop_end;
 }
 
 stride_status check_domains(const double *table, int32_t n_dom, const char *name) {
@@ -121,8 +129,11 @@ stride_status stride_score(const stride_layout *layout, int32_t vocab, int64_t l
                     STRIDE_MAX_DOMAINS);
     if (!student_logits && (logp_s || kl || kl_full))
         return fail(STRIDE_ERR_INVALID_ARG, "logp_s / kl / kl_full requested without student logits");
-    if (kl_full && !logp_s && L.n_tokens > 0)
-        return fail(STRIDE_ERR_INVALID_ARG, "kl_full needs logp_s as well");
+    // the student rows' results are written to logp_s, and kl is formed from it
+    if (student_logits && !logp_s && L.n_tokens > 0)
+        return fail(STRIDE_ERR_INVALID_ARG, "student_logits given without logp_s");
+    if ((kl || kl_full) && !logp_s && L.n_tokens > 0)
+        return fail(STRIDE_ERR_INVALID_ARG, "kl / kl_full need logp_s as well");
     if (L.n_tokens > 0) {
         if (!teacher_logits) return fail(STRIDE_ERR_INVALID_ARG, "teacher_logits is NULL");
         for (int d = 0; d < n_teachers; ++d) {
@@ -139,7 +150,7 @@ stride_status stride_score(const stride_layout *layout, int32_t vocab, int64_t l
     if (L.n_turns > 0 && !turn_mean) return fail(STRIDE_ERR_INVALID_ARG, "turn_mean is NULL");
     const bool routed = n_teachers > 1 && L.domain != nullptr;
     if (routed) {
-        st = check_ws(layout, 0, ws, ws_bytes);
+        st = check_ws(rows_ws_bytes(L), ws, ws_bytes);
         if (st != STRIDE_OK) return st;
     }
 
@@ -184,6 +195,8 @@ stride_status stride_score_fused(const stride_layout *layout, int32_t vocab, int
                     "hidden size d = %d is not a multiple of 64 in [64, %d]", d, kMaxFusedD);
     if (!student_logits && (logp_s || kl))
         return fail(STRIDE_ERR_INVALID_ARG, "logp_s / kl requested without student logits");
+    if (student_logits && !logp_s && L.n_tokens > 0)
+        return fail(STRIDE_ERR_INVALID_ARG, "student_logits given without logp_s");
     if (L.n_tokens > 0) {
         if (!hidden_t || !w_t) return fail(STRIDE_ERR_INVALID_ARG, "hidden_t or w_t is NULL");
         if (!aligned(hidden_t, 16) || !aligned(w_t, 16))
@@ -235,7 +248,7 @@ stride_status stride_stop(const stride_layout *layout, int32_t unit, const void 
     if (n_units > 0 && (!values || !cum))
         return fail(STRIDE_ERR_INVALID_ARG, "values or cum is NULL");
     if (L.n_rollouts > 0 && !stop_unit) return fail(STRIDE_ERR_INVALID_ARG, "stop_unit is NULL");
-    st = check_ws(layout, n_units, ws, ws_bytes);
+    st = check_ws(stop_ws_bytes(L, n_units), ws, ws_bytes);
     if (st != STRIDE_OK) return st;
     DomainTable lt{};
     for (int i = 0; i < n_dom; ++i) lt.v[i] = lambda[i];
@@ -315,7 +328,7 @@ stride_status stride_opd_grad(const stride_layout *layout, int32_t unit, int32_t
         if (!aligned(student_logits, 16) || !aligned(grad, 16))
             return fail(STRIDE_ERR_UNSUPPORTED, "student_logits and grad must be 16-byte aligned");
     }
-    st = check_ws(layout, 0, ws, ws_bytes);
+    st = check_ws(rows_ws_bytes(L), ws, ws_bytes);
     if (st != STRIDE_OK) return st;
     const WsLayout w = ws_layout(L.n_rollouts, L.n_tokens, 0, 0);
     uint8_t *mask = static_cast<uint8_t *>(ws) + w.row_dom;
@@ -337,6 +350,34 @@ stride_status stride_probe_read(const void *a, const void *b, int64_t n_rows, in
     if (row_bytes % 16 != 0 || !aligned(a, 16) || (b && !aligned(b, 16)))
         return fail(STRIDE_ERR_UNSUPPORTED, "rows must be 16-byte aligned");
     hipError_t e = launch_probe_read(a, b, n_rows, row_bytes, read_bytes, sink, stream);
+    if (e != hipSuccess) return hip_fail(e, "probe launch");
+    return ok();
+}
+
+stride_status stride_probe_read_flat(const void *a, const void *b, int64_t n_bytes, uint32_t *sink,
+                                     int64_t sink_len, hipStream_t stream) {
+    if (n_bytes < 0) return fail(STRIDE_ERR_INVALID_ARG, "n_bytes = %lld < 0", (long long)n_bytes);
+    if (n_bytes == 0) return ok();
+    if (!a || !sink) return fail(STRIDE_ERR_INVALID_ARG, "a or sink is NULL");
+    if (sink_len < 4) return fail(STRIDE_ERR_INVALID_ARG, "sink_len = %lld < 4", (long long)sink_len);
+    if (n_bytes % 16 != 0 || !aligned(a, 16) || (b && !aligned(b, 16)))
+        return fail(STRIDE_ERR_UNSUPPORTED, "ranges must be 16-byte aligned multiples of 16 bytes");
+    hipError_t e = launch_probe_flat(a, b, n_bytes, sink, sink_len, stream);
+    if (e != hipSuccess) return hip_fail(e, "probe launch");
+    return ok();
+}
+
+stride_status stride_probe_copy(const void *src, void *dst, const uint8_t *row_mask, int64_t n_rows,
+                                int64_t row_bytes, int64_t copy_bytes, hipStream_t stream) {
+    if (n_rows < 0) return fail(STRIDE_ERR_INVALID_ARG, "n_rows = %lld < 0", (long long)n_rows);
+    if (n_rows == 0) return ok();
+    if (!src || !dst) return fail(STRIDE_ERR_INVALID_ARG, "src or dst is NULL");
+    if (copy_bytes < 16 || copy_bytes > row_bytes)
+        return fail(STRIDE_ERR_INVALID_ARG, "copy_bytes = %lld outside [16, row_bytes = %lld]",
+                    (long long)copy_bytes, (long long)row_bytes);
+    if (row_bytes % 16 != 0 || !aligned(src, 16) || !aligned(dst, 16))
+        return fail(STRIDE_ERR_UNSUPPORTED, "rows must be 16-byte aligned");
+    hipError_t e = launch_probe_copy(src, dst, row_mask, n_rows, row_bytes, copy_bytes, stream);
     if (e != hipSuccess) return hip_fail(e, "probe launch");
     return ok();
 }

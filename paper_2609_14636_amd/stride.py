@@ -17,6 +17,8 @@ import torch
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libstride.so")
+# the same library with the stop test's look-back delay hook compiled in (tests only)
+DEBUG_LIB_PATH = os.path.join(HERE, "libstride_debug.so")
 
 STRIDE_OK = 0
 STRIDE_BF16, STRIDE_F32 = 0, 1
@@ -67,11 +69,11 @@ class _CLayout(ctypes.Structure):
                 ("turn_tok_off", ctypes.c_void_p), ("domain", ctypes.c_void_p)]
 
 
-def _load():
-    if not os.path.exists(LIB_PATH):
-        raise ImportError(f"{LIB_PATH} is missing: build it with "
+def _load(path: str = LIB_PATH):
+    if not os.path.exists(path):
+        raise ImportError(f"{path} is missing: build it with "
                           "`python paper_2609_14636_amd/csrc/build.py` (no other code path exists)")
-    lib = ctypes.CDLL(LIB_PATH)
+    lib = ctypes.CDLL(path)
     vp, i32, i64, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
     lp = ctypes.POINTER(_CLayout)
     lib.stride_workspace_size.argtypes = [lp, i32]
@@ -107,6 +109,12 @@ def _load():
     lib.stride_records_plan.restype = i32
     lib.stride_probe_read.argtypes = [vp, vp, i64, i64, i64, vp, vp]
     lib.stride_probe_read.restype = i32
+    lib.stride_probe_read_flat.argtypes = [vp, vp, i64, vp, i64, vp]
+    lib.stride_probe_read_flat.restype = i32
+    lib.stride_probe_copy.argtypes = [vp, vp, vp, i64, i64, i64, vp]
+    lib.stride_probe_copy.restype = i32
+    lib.stride_debug_scan_delay.argtypes = [ctypes.c_uint64, ctypes.c_uint32, ctypes.c_uint32]
+    lib.stride_debug_scan_delay.restype = i32
     lib.stride_last_error.argtypes = []
     lib.stride_last_error.restype = ctypes.c_char_p
     return lib
@@ -117,6 +125,12 @@ _lib = _load()
 
 def library() -> ctypes.CDLL:
     return _lib
+
+
+def debug_library() -> ctypes.CDLL:
+    """libstride_debug.so (the stop test's look-back delay hook compiled in), with the same
+    argument types; for tests of the cross-workgroup protocol only."""
+    return _load(DEBUG_LIB_PATH)
 
 
 def _ptr(t: torch.Tensor | None) -> int | None:
@@ -273,6 +287,24 @@ def stride_probe_read(a: torch.Tensor, b: torch.Tensor | None, read_bytes: int,
         raise ValueError("a and b must share shape, dtype and strides")
     _check(_lib.stride_probe_read(_ptr(a), _ptr(b), a.shape[0], a.stride(0) * a.element_size(),
                                   int(read_bytes), _ptr(sink), _stream(stream)))
+
+
+def stride_probe_read_flat(a: torch.Tensor, b: torch.Tensor | None, n_bytes: int,
+                           sink: torch.Tensor, stream=None) -> None:
+    """Streaming-read reference in grid-stride order over the first n_bytes of a (and b)."""
+    _check(_lib.stride_probe_read_flat(_ptr(a), _ptr(b), int(n_bytes), _ptr(sink), sink.numel(),
+                                       _stream(stream)))
+
+
+def stride_probe_copy(src: torch.Tensor, dst: torch.Tensor, row_mask: torch.Tensor | None,
+                      copy_bytes: int, stream=None) -> None:
+    """Read+write reference: copies the first copy_bytes of every row of src to dst (rows with a
+    0 mask byte are zero-filled without a read), the OPD gradient's access pattern."""
+    if dst.stride() != src.stride() or dst.shape != src.shape or dst.dtype != src.dtype:
+        raise ValueError("src and dst must share shape, dtype and strides")
+    _check(_lib.stride_probe_copy(_ptr(src), _ptr(dst), _ptr(row_mask), src.shape[0],
+                                  src.stride(0) * src.element_size(), int(copy_bytes),
+                                  _stream(stream)))
 
 
 class Records:

@@ -200,6 +200,15 @@ class Workload:
         self._fill_host(out, d, d, BF16, 0, v, STREAM_W, self.w_sigma, None, None, threads)
         return out
 
+    def w_dv_host(self, threads: int = 8) -> np.ndarray:
+        """The same lm_head bits as the [d, V] matrix of z = h W (the transpose of w_host),
+        copied in blocks of 256 vocabulary rows so that the copy stays cache-friendly."""
+        w = self.w_host(threads)
+        out = np.empty((w.shape[1], w.shape[0]), np.uint16)
+        for i in range(0, w.shape[0], 256):
+            out[:, i:i + 256] = w[i:i + 256].T
+        return out
+
     # ---------------------------------------------------------- device fills
     def fill_device(self, ptr: int, cols: int, ld: int, dtype: int, row0: int, n: int, stream: int,
                     sigma: float, tok_dev: int | None, boost_dev: int | None, hip_stream: int):

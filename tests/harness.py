@@ -102,18 +102,25 @@ def run_gpu_fused(wl: W.Workload, lam, alpha, inp=None):
     return path.host()
 
 
-def oracle_fused_scores(wl: W.Workload, rows, w_dv=None, threads: int = 16):
+def oracle_fused_scores(wl: W.Workload, rows, w_dv=None, threads: int = 16, matmul: bool = False):
     """Oracle teacher/student log-probabilities of the given rows of a fused workload.
     The oracle takes the lm_head as the [d, V] matrix of z = h W, the transpose of the
-    [V, d] storage the GPU reads; both come from the host generator."""
+    [V, d] storage the GPU reads; both come from the host generator.  With ``matmul`` the
+    projection is the oracle's library-matmul form (for whole rollouts at full size)."""
     if w_dv is None:
-        w_dv = np.ascontiguousarray(wl.w_host(threads).T)
+        w_dv = wl.w_dv_host(threads)
     rows = np.asarray(rows, np.int64)
-    h = np.concatenate([wl.hidden_host(int(r), 1, 1) for r in rows]) if rows.size else \
-        np.zeros((0, wl.fused_d), np.uint16)
+    contiguous = rows.size > 0 and np.array_equal(rows, np.arange(rows[0], rows[0] + rows.size))
+    if contiguous:
+        h = wl.hidden_host(int(rows[0]), rows.size, threads)
+        s = wl.student_rows_host(int(rows[0]), rows.size, threads)
+    else:
+        h = np.concatenate([wl.hidden_host(int(r), 1, 1) for r in rows]) if rows.size else \
+            np.zeros((0, wl.fused_d), np.uint16)
+        s = np.concatenate([wl.student_rows_host(int(r), 1, 1) for r in rows])
     ids = wl.tok[rows]
-    lt, _, ft = OP.O.fused_logp(h, w_dv, ids)
-    s = np.concatenate([wl.student_rows_host(int(r), 1, 1) for r in rows])
+    fused = OP.O.fused_logp_matmul if matmul else OP.O.fused_logp
+    lt, _, ft = fused(h, w_dv, ids)
     ls, _, fs = OP.O.logp_rows(s, ids, wl.vocab)
     return {"logp_t": lt, "logp_s": ls, "kl": OP.O.token_kl(ls, lt), "flags": ft | fs}, w_dv
 

@@ -296,6 +296,33 @@ def check_fused_against_matmul():
         assert abs(got[i] - _decimal_logp(z[i], ids[i])) < 1e-12
 
 
+def check_fused_matmul_form():
+    """fused_logp_matmul (library matmul, then the row log-softmax) equals fused_logp on shapes
+    where no two sizes are equal, with W given both as a [d, V] array and as the transposed view
+    of its [V, d] storage, across several row blocks; and the 50-digit brute force."""
+    rng = np.random.default_rng(41)
+    n, d, vocab = 7, 40, 53
+    h = _bf16_bits(rng.normal(0, 1, size=(n, d)).astype(np.float32))
+    w_vd = _bf16_bits(rng.normal(0, 0.3, size=(vocab, d)).astype(np.float32))
+    ids = rng.integers(0, vocab, size=n).astype(np.int32)
+    want, want_lse, f0 = O.fused_logp(h, np.ascontiguousarray(w_vd.T), ids)
+    assert f0 == 0
+    for w in (np.ascontiguousarray(w_vd.T), w_vd.T):
+        for block in (1, 3, 256):
+            got, got_lse, flags = O.fused_logp_matmul(h, w, ids, rows_per_call=block)
+            assert flags == 0
+            assert np.allclose(got, want, rtol=0, atol=1e-12)
+            assert np.allclose(got_lse, want_lse, rtol=0, atol=1e-12)
+    z = _bf16_to_f32(h).astype(np.float64) @ _bf16_to_f32(w_vd).astype(np.float64).T
+    got, _, _ = O.fused_logp_matmul(h, w_vd.T, ids)
+    for i in range(n):
+        assert abs(got[i] - _decimal_logp(z[i], ids[i])) < 1e-12
+    bad = ids.copy()
+    bad[2] = vocab
+    _, _, flags = O.fused_logp_matmul(h, w_vd.T, bad)
+    assert flags & O.FLAG_TOKEN_OOB
+
+
 ALL_CHECKS = [
     check_logp_brute_force,
     check_logp_uniform_closed_form,
@@ -312,6 +339,7 @@ ALL_CHECKS = [
     check_restart_golden,
     check_restart_brute_force,
     check_fused_against_matmul,
+    check_fused_matmul_form,
 ]
 
 

@@ -64,6 +64,10 @@ def _fake(n):
     ("vocab0", P.stride.StrideError), ("ld_small", P.stride.StrideError),
     ("bad_unit", P.stride.StrideError), ("ws_small", P.stride.StrideError),
     ("n_dom0", P.stride.StrideError), ("kl_without_student", P.stride.StrideError),
+    ("student_without_logp_s", P.stride.StrideError), ("kl_without_logp_s", P.stride.StrideError),
+    ("kl_full_without_logp_s", P.stride.StrideError),
+    ("fused_student_without_logp_s", P.stride.StrideError),
+    ("fused_kl_without_logp_s", P.stride.StrideError),
 ])
 def test_argument_errors_raise_before_launch(case, status):
     lay = _layout()
@@ -87,7 +91,22 @@ def test_argument_errors_raise_before_launch(case, status):
                                   None, stream=0)
         elif case == "kl_without_student":
             P.stride_score(lay, 16, [x], None, ids, out, None, out, tm, None, ws, stream=0)
-    assert ei.value.status in (1, 2, 3)
+        elif case == "student_without_logp_s":
+            # the student rows' log-probabilities would be written through logp_s
+            P.stride_score(lay, 16, [x], x, ids, out, None, None, tm, None, ws, stream=0)
+        elif case == "kl_without_logp_s":
+            P.stride_score(lay, 16, [x], x, ids, out, None, out, tm, None, ws, stream=0)
+        elif case == "kl_full_without_logp_s":
+            P.stride_score(lay, 16, [x], x, ids, out, None, None, tm, None, ws, stream=0,
+                           kl_full=out)
+        elif case in ("fused_student_without_logp_s", "fused_kl_without_logp_s"):
+            h = torch.zeros((10, 64), dtype=torch.bfloat16)
+            w = torch.zeros((16, 64), dtype=torch.bfloat16)
+            xs = torch.zeros((10, 16), dtype=torch.bfloat16)
+            kl = out if case == "fused_kl_without_logp_s" else None
+            P.stride_score_fused(lay, 16, h, w, xs, ids, out, None, kl, tm, None, ws, stream=0)
+    assert ei.value.status == (3 if case == "ws_small" else (2 if case == "n_dom0" else 1)), \
+        P.library().stride_last_error().decode()
     assert P.library().stride_last_error().decode()
 
 
@@ -137,3 +156,4 @@ def test_flag_word_decoding():
     assert P.flag_names(1 << 20) == [hex(1 << 20)]
     err = P.StrideDataError(P.STRIDE_FLAG_EMPTY_TURN | P.STRIDE_FLAG_SPIN_LIMIT)
     assert "EMPTY_TURN" in str(err) and "SPIN_LIMIT" in str(err) and err.flags == 34
+

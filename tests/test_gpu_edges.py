@@ -172,3 +172,27 @@ def test_fused_confident_teacher_log_probability_is_at_most_zero():
     assert fl == 0 and np.max(want) <= 0
     assert np.max(np.abs(got - want)) <= H.TOL_LOGP, np.max(np.abs(got - want))
     say(f"[fused confident] logp in [{got.min():.2e}, {got.max():.2e}], max |d| {np.max(np.abs(got - want)):.2e}")
+
+
+def test_single_teacher_reads_teacher_zero_whatever_the_domain_ids():
+    """With one teacher every row reads teacher 0; the rollouts' domain ids are not used by
+    stride_score (they select lambda and alpha in the stop and restart calls, which check them).
+    Scoring with domain ids 0..3 gives the same bits as scoring without any, and no flag."""
+    import torch
+    import paper_2609_14636_amd as P
+    wl = W.make("agentic", seed=31, scale=dict(R=4, turns=3, tok_lo=20, tok_hi=70, vocab=1000))
+    inp = H.device_inputs(wl)
+    lay0 = inp["layout"]
+    dom = torch.arange(wl.n_rollouts, dtype=torch.int32, device="cuda")
+    lay1 = P.Layout(lay0.rollout_turn_off, lay0.turn_tok_off, wl.n_tokens, dom)
+    outs = []
+    for lay in (lay0, lay1):
+        path = P.Path(lay, wl.unit, with_student=True)
+        path.score(wl.vocab, inp["teachers"], inp["student"], inp["ids"])
+        torch.cuda.synchronize()
+        h = path.host()
+        assert h["flags"] == 0, P.flag_names(h["flags"])
+        outs.append(h)
+    say(f"[single teacher] R={wl.n_rollouts} N={wl.n_tokens}: domain ids 0..{wl.n_rollouts - 1}")
+    for k in ("logp_t", "logp_s", "kl", "turn_mean"):
+        assert np.array_equal(outs[0][k].view(np.uint8), outs[1][k].view(np.uint8)), k

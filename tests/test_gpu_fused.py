@@ -65,28 +65,37 @@ def test_fused_parity(R, turns, tok, vocab, d):
 
 
 def test_fused_full_size():
-    """The fused workload at full size (65,536 rows, d = 2048, V = 151,936)."""
+    """The fused workload at full size (65,536 rows, d = 2048, V = 151,936): one whole rollout
+    (4,096 rows, 8 turns) against the oracle -- every row's log-probabilities and KL, its turn
+    means, cumulative sums, stop, k*, K0 and K_max -- plus scattered rows of other rollouts and
+    tiles, and properties that hold for every rollout."""
+    import time
     wl = W.make("fused", 1001)
     lam, alpha = WP.fused_thresholds(wl.vocab, wl.fused_d, wl.hidden_sigma, wl.w_sigma)
     gpu = H.run_gpu_fused(wl, lam, alpha)
     assert gpu["flags"] == 0, hex(gpu["flags"])
     H.assert_invariants(gpu, wl)
-    # one complete turn (rows of turn 5 of rollout 3) plus scattered rows, element by element
-    t = int(wl.rollout_turn_off[3]) + 5
-    a, b = int(wl.turn_tok_off[t]), int(wl.turn_tok_off[t + 1])
+    t0 = time.time()
+    w_dv = wl.w_dv_host(16)
+    r = 3
+    a, b = wl.rollout_rows(r)
+    sc, _ = H.oracle_fused_scores(wl, np.arange(a, b), w_dv=w_dv, matmul=True)
+    assert sc["flags"] == 0
+    say(f"[fused full] oracle on rollout {r} ({b - a} rows): {time.time() - t0:.1f} s")
+    ora = {r: (sc, H.oracle_rollout(wl, r, sc, lam, alpha))}
+    rep = H.compare(wl, gpu, ora, lam, alpha)
+    say(f"[fused full] rollout {r}: {rep}")
+    assert rep.stop_excused == 0 and rep.restart_excused == 0
+    # scattered rows of other rollouts and tiles (the first and last rows, tile edges)
     extra = np.array([0, 1, 255, 256, 4095, 32768, wl.n_tokens - 1])
-    rows = np.concatenate([np.arange(a, b), extra])
-    sc, _ = H.oracle_fused_scores(wl, rows)
+    sx, _ = H.oracle_fused_scores(wl, extra, w_dv=w_dv)
     for k in ("logp_t", "logp_s"):
-        d = np.max(np.abs(gpu[k][rows] - sc[k]))
+        d = np.max(np.abs(gpu[k][extra] - sx[k]))
         assert d <= H.TOL_LOGP, (k, d)
-        say(f"[fused full] max |d {k}| over {rows.size} rows = {d:.2e}")
-    d = np.max(np.abs(gpu["kl"][rows] - sc["kl"]))
+    d = np.max(np.abs(gpu["kl"][extra] - sx["kl"]))
     assert d <= H.TOL_KL, d
-    turn = math.fsum(sc["logp_t"][:b - a]) / (b - a)
-    assert abs(gpu["turn_mean"][t] - turn) <= H.TOL_LOGP, (gpu["turn_mean"][t], turn)
-    # every turn mean sits near the closed form -(log V + d s_h^2 s_W^2 / 2), so with
-    # lambda = 5.5 x that value every rollout stops on its sixth turn (index 5)
+    # every turn mean sits near the closed form -(log V + d s_h^2 s_W^2 / 2), and lambda is
+    # 5.5 times that value, so every rollout stops on its sixth turn (index 5)
     expect = lam[0] / 5.5
     assert np.all(np.abs(gpu["turn_mean"] - expect) < 0.5), (gpu["turn_mean"].min(), expect)
     assert gpu["stop_unit"].tolist() == [5] * wl.n_rollouts, gpu["stop_unit"]
