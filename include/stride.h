@@ -185,6 +185,27 @@ stride_status stride_stop(const stride_layout *layout, int32_t unit, const void 
                           uint32_t *dev_flags, void *ws, size_t ws_bytes, hipStream_t stream);
 
 /*
+ * stride_stop without a workspace, for callers that cannot allocate device memory
+ * (code under HIP graph capture, tight serving loops, harnesses that forbid
+ * allocation).  Arguments, outputs and errors are those of stride_stop without
+ * ws / ws_bytes.  The call allocates nothing: its scratch (tile counter, unit
+ * offsets, scan tile descriptors; 256 + 8 (R + 1) + 16 ceil(U / 2048) bytes, each
+ * part rounded up to 256) lives in a fixed device array of
+ * STRIDE_NOALLOC_SCRATCH_BYTES per GPU, which the library holds until the process
+ * ends (for example R = 65,536 rollouts with up to 67 million units fit).  A layout
+ * that needs more returns STRIDE_ERR_UNSUPPORTED before any launch.  The first call
+ * on each device looks up that device's array address.  Every call on one GPU
+ * shares the array, which keeps the last call's contents; the call clears what must
+ * start at zero with its own kernel, in stream order.  Calls that overlap on one
+ * GPU (unordered streams, or several host threads) race: order them.
+ */
+#define STRIDE_NOALLOC_SCRATCH_BYTES (1u << 20)
+stride_status stride_stop_noalloc(const stride_layout *layout, int32_t unit, const void *values,
+                                  const double *lambda, int32_t n_dom, const int32_t *start_unit,
+                                  double *cum, int32_t *stop_unit, int64_t *n_retained_tokens,
+                                  uint32_t *dev_flags, hipStream_t stream);
+
+/*
  * Online form of the stop test, for use while rollouts are being generated
  * (Algorithm 1's inner loop: after each new turn the teacher scores it and the
  * sum over the new turns is tested against lambda, Eq. 5).  Each call appends new
@@ -327,7 +348,7 @@ stride_status stride_probe_copy(const void *src, void *dst, const uint8_t *row_m
 /* Test hook of the stop test's cross-workgroup look-back (not a step of the method).
  *
  * In the library built for testing (libstride_debug.so, scan compiled with
- * STRIDE_SCAN_DELAY_HOOK), later stride_stop calls make the scan tiles
+ * STRIDE_SCAN_DELAY_HOOK), later stride_stop / stride_stop_noalloc calls make the scan tiles
  * picked by a hash of (seed, tile) -- about one in `one_in` -- sleep 1 .. `sleeps` times
  * s_sleep(127) (about 8,000 cycles each) before publishing their aggregate, so that their
  * successors look back over descriptors that are not yet published.  The waits stay far below

@@ -11,5 +11,5 @@ from .stride import (  # noqa: F401
     library,
     stride_fused_workspace_size, stride_opd_grad, stride_probe_copy, stride_probe_read,
     stride_probe_read_flat, stride_restart_turn,
-    stride_score, stride_score_fused, stride_stop, stride_stop_step,
+    stride_score, stride_score_fused, stride_stop, stride_stop_noalloc, stride_stop_step,
     stride_workspace_size)

@@ -80,6 +80,9 @@ hipError_t launch_stop(const stride_layout &L, int32_t unit, const void *values,
                        const DomainTable &lambda, int32_t n_dom, const int32_t *start,
                        double *cum, int32_t *stop_unit, int64_t *retained, uint32_t *flags,
                        void *ws, hipStream_t stream);
+// Device address of this GPU's fixed scratch array (STRIDE_NOALLOC_SCRATCH_BYTES), looked
+// up on the first call per device.
+hipError_t noalloc_scratch(void **ptr);
 
 // fused.hip
 size_t fused_ws_bytes(int64_t n_rows, int32_t vocab);

@@ -26,6 +26,7 @@
 // STRIDE_FLAG_SPIN_LIMIT and writes NaN, so no wave can hang.
 #include <atomic>
 #include <climits>
+#include <mutex>
 
 #include "common.hpp"
 
@@ -438,6 +439,37 @@ hipError_t launch_stop(const stride_layout &L, int32_t unit, const void *values,
         e = hipGetLastError();
     }
     return e;
+}
+
+// ---- scratch of the allocation-free stop test ----
+// A fixed device array, one copy per GPU, held until the process ends.  In host code
+// `scratch` names a host-side stand-in, not a device address: the device address of each
+// GPU's copy comes from hipGetSymbolAddress, looked up once per device with that device
+// current, and only that address is handed to kernels.
+static __device__ __align__(256) char scratch[STRIDE_NOALLOC_SCRATCH_BYTES];
+
+constexpr int kMaxDevices = 64;
+
+hipError_t noalloc_scratch(void **ptr) {
+    static std::atomic<void *> addr[kMaxDevices];
+    static std::mutex mu;
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    void *p = addr[dev].load(std::memory_order_acquire);
+    if (!p) {
+        std::lock_guard<std::mutex> g(mu);
+        p = addr[dev].load(std::memory_order_relaxed);
+        if (!p) {
+            e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+            if (e != hipSuccess) return e;
+            if (!p) return hipErrorInvalidSymbol;
+            addr[dev].store(p, std::memory_order_release);
+        }
+    }
+    *ptr = p;
+    return hipSuccess;
 }
 
 }  // namespace stride

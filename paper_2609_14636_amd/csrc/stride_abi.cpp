@@ -258,6 +258,39 @@ stride_status stride_stop(const stride_layout *layout, int32_t unit, const void 
     return ok();
 }
 
+stride_status stride_stop_noalloc(const stride_layout *layout, int32_t unit, const void *values,
+                                  const double *lambda, int32_t n_dom, const int32_t *start_unit,
+                                  double *cum, int32_t *stop_unit, int64_t *n_retained_tokens,
+                                  uint32_t *dev_flags, hipStream_t stream) {
+    stride_status st = check_layout(layout);
+    if (st != STRIDE_OK) return st;
+    const stride_layout &L = *layout;
+    if (unit != STRIDE_UNIT_TURN && unit != STRIDE_UNIT_TOKEN)
+        return fail(STRIDE_ERR_INVALID_ARG, "unit %d is neither STRIDE_UNIT_TURN nor STRIDE_UNIT_TOKEN",
+                    unit);
+    st = check_domains(lambda, n_dom, "lambda");
+    if (st != STRIDE_OK) return st;
+    const int64_t n_units = (unit == STRIDE_UNIT_TURN) ? L.n_turns : L.n_tokens;
+    if (n_units > 0 && (!values || !cum))
+        return fail(STRIDE_ERR_INVALID_ARG, "values or cum is NULL");
+    if (L.n_rollouts > 0 && !stop_unit) return fail(STRIDE_ERR_INVALID_ARG, "stop_unit is NULL");
+    const size_t need = stop_ws_bytes(L, n_units);
+    if (need > (size_t)STRIDE_NOALLOC_SCRATCH_BYTES)
+        return fail(STRIDE_ERR_UNSUPPORTED,
+                    "layout needs %zu bytes of scratch (R = %d, %lld units); the fixed scratch "
+                    "holds %zu: use stride_stop with a workspace",
+                    need, L.n_rollouts, (long long)n_units, (size_t)STRIDE_NOALLOC_SCRATCH_BYTES);
+    void *scratch = nullptr;
+    hipError_t e = noalloc_scratch(&scratch);
+    if (e != hipSuccess) return hip_fail(e, "scratch address lookup");
+    DomainTable lt{};
+    for (int i = 0; i < n_dom; ++i) lt.v[i] = lambda[i];
+    e = launch_stop(L, unit, values, lt, n_dom, start_unit, cum, stop_unit, n_retained_tokens,
+                    dev_flags, scratch, stream);
+    if (e != hipSuccess) return hip_fail(e, "stop launch");
+    return ok();
+}
+
 stride_status stride_stop_step(int32_t n_active, const int32_t *slot, const int64_t *new_off,
                                int32_t unit, const void *values, const int32_t *domain,
                                const double *lambda, int32_t n_dom, double *state_cum,

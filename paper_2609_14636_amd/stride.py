@@ -93,6 +93,8 @@ def _load(path: str = LIB_PATH):
     lib.stride_opd_grad.argtypes = [lp, i32, i32, i64, i32, vp, vp, vp, vp, vp, vp, ctypes.c_float,
                                     vp, vp, vp, vp, sz, vp]
     lib.stride_opd_grad.restype = i32
+    lib.stride_stop_noalloc.argtypes = [lp, i32, vp, vp, i32, vp, vp, vp, vp, vp, vp]
+    lib.stride_stop_noalloc.restype = i32
     lib.stride_stop_step.argtypes = [i32, vp, vp, i32, vp, vp, vp, i32, vp, vp, vp, vp, vp]
     lib.stride_stop_step.restype = i32
     lib.stride_records_create.argtypes = []
@@ -240,6 +242,17 @@ def stride_stop(layout: Layout, unit: int, values: torch.Tensor, lam: Sequence[f
                             len(lam), _ptr(start_unit), _ptr(cum), _ptr(stop_unit),
                             _ptr(n_retained_tokens), _ptr(dev_flags), _ptr(ws),
                             ws.numel() * ws.element_size(), _stream(stream)))
+
+
+def stride_stop_noalloc(layout: Layout, unit: int, values: torch.Tensor, lam: Sequence[float],
+                        start_unit: torch.Tensor | None, cum: torch.Tensor, stop_unit: torch.Tensor,
+                        n_retained_tokens: torch.Tensor | None, dev_flags: torch.Tensor | None,
+                        stream=None) -> None:
+    """stride_stop with its scratch in the library's fixed per-GPU array (no workspace)."""
+    lt = _doubles(lam)
+    _check(_lib.stride_stop_noalloc(layout.c(), unit, _ptr(values), ctypes.cast(lt, ctypes.c_void_p),
+                                    len(lam), _ptr(start_unit), _ptr(cum), _ptr(stop_unit),
+                                    _ptr(n_retained_tokens), _ptr(dev_flags), _stream(stream)))
 
 
 def stride_stop_step(slot: torch.Tensor, new_off: torch.Tensor, unit: int, values: torch.Tensor,

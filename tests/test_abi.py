@@ -157,3 +157,17 @@ def test_flag_word_decoding():
     err = P.StrideDataError(P.STRIDE_FLAG_EMPTY_TURN | P.STRIDE_FLAG_SPIN_LIMIT)
     assert "EMPTY_TURN" in str(err) and "SPIN_LIMIT" in str(err) and err.flags == 34
 
+
+def test_noalloc_stop_rejects_layouts_past_its_fixed_scratch():
+    """stride_stop_noalloc keeps its scratch in a fixed per-GPU array; a layout whose tile
+    counter, unit offsets and scan descriptors do not fit returns STRIDE_ERR_UNSUPPORTED on the
+    host, before the array is looked up or anything is launched."""
+    R = 200_000  # 8 (R + 1) bytes of unit offsets alone exceed the array
+    lay = P.Layout(torch.zeros(R + 1, dtype=torch.int32), torch.zeros(2, dtype=torch.int64), 10)
+    tm = torch.zeros(1, dtype=torch.float64)
+    stop = torch.zeros(R, dtype=torch.int32)
+    with pytest.raises(P.StrideError) as ei:
+        P.stride_stop_noalloc(lay, P.STRIDE_UNIT_TURN, tm, [-1.0], None, tm, stop, None, None,
+                              stream=0)
+    assert ei.value.status == 2
+    assert "scratch" in P.library().stride_last_error().decode()
