@@ -12,12 +12,18 @@
 //   of four (one wave per SIMD) that alternate every 32-wide K step: while one
 //   group multiplies from registers, the other reads its next fragments from LDS
 //   and issues loads, then a barrier swaps them (ping-pong), so each SIMD's matrix
-//   unit always has a wave with work.  K = d streams through two 64-wide LDS
-//   stages filled by direct buffer->LDS loads (buffer_load_dwordx4 ... lds, no
-//   register staging); eight lanes load one row's 128 bytes, a whole cache line,
-//   and rows are XOR-swizzled so the 16-byte fragment reads are free of bank
-//   conflicts.  Both operands are K-contiguous, so each MFMA operand is one
-//   16-byte LDS read.  W is the A operand and H the B operand, so each lane's
+//   unit always has a wave with work.  K = d streams in 64-wide stages through a
+//   ring of five 32 KB LDS buffers (the whole 160 KB LDS), each holding one
+//   operand of one stage, filled by direct buffer->LDS loads (buffer_load_dwordx4
+//   ... lds, no register staging): H of stage j in buffer 2j mod 5, W in 2j+1 mod 5.
+//   Every memory phase issues one operand's loads -- W(j+1) in the first half of
+//   stage j, H(j+2) in the second -- so the loads are spread evenly over the
+//   phases and each has two to four phases to land.  Eight lanes load one row's
+//   128 bytes, a whole cache line, and rows are XOR-swizzled so the 16-byte
+//   fragment reads are free of bank conflicts.  No vector ALU work remains in the
+//   loop: wave-uniform values are scalar and the fragment addresses are fixed per
+//   buffer.  Both operands are K-contiguous, so each MFMA operand is one 16-byte
+//   LDS read.  W is the A operand and H the B operand, so each lane's
 //   accumulators hold 64 of one token's 128 logits and its partner lane (l ^ 32)
 //   the other 64: the epilogue reduces a token to (max, sum of exp(z - max)) with
 //   one exchange and writes it to a partial table [V/128][N] (tokens contiguous).
@@ -44,13 +50,12 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 #define LDS_PTR(p) ((__attribute__((address_space(3))) void *)(p))
 
-constexpr int kBM = 256, kBN = 256, kBK = 64;      // tile and LDS stage width
-constexpr int kStages = 2;
+constexpr int kBM = 256, kBN = 256, kBK = 64;      // tile and stage width along K
 constexpr int kThreads = 512;                      // eight waves
 constexpr int kRowB = kBK * 2;                     // 128 bytes per LDS row
-constexpr int kTileB = kBM * kRowB;                // 32 KB per operand tile
-constexpr int kStageB = 2 * kTileB;                // 64 KB per stage
-constexpr size_t kLdsBytes = (size_t)kStages * kStageB;
+constexpr int kBufB = kBM * kRowB;                 // 32 KB: one operand of one stage
+constexpr int kBuffers = 5;                        // LDS ring of operand buffers
+constexpr size_t kLdsBytes = (size_t)kBuffers * kBufB;  // 160 KB, the whole LDS
 constexpr int kHalf = 128;                         // vocabulary entries per partial
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.69314718055994531f;
@@ -101,7 +106,9 @@ __device__ __forceinline__ void barrier() {
 
 __global__ __launch_bounds__(kThreads, 1) void fused_lse_kernel(FusedArgs a) {
     extern __shared__ __attribute__((aligned(1024))) char lds[];
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int tid = threadIdx.x, lane = tid & 63;
+    // wave-uniform values in scalar registers: the LDS-DMA destinations are scalar arithmetic
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int grp = wave >> 2;                   // ping-pong group (one wave per SIMD)
     const int wv = wave & 1, wt = wave >> 1;     // vocabulary half, token quarter
 
@@ -117,12 +124,12 @@ __global__ __launch_bounds__(kThreads, 1) void fused_lse_kernel(FusedArgs a) {
     const int64_t n0 = (int64_t)tn * kBN;
     const int d = a.d, ns = d / kBK;
 
-    // ---- direct global -> LDS loads (buffer_load_dwordx4 ... lds): each wave fills 32
-    // rows of each operand per stage, 8 rows per instruction (lane l -> row l >> 3,
-    // position l & 7 of the swizzled row).  Each operand's descriptor spans only the
-    // rows of this tile that exist, so rows past N or V read as zeros (their results
-    // are never used) and no load can leave the operand.  Lane offsets are 32-bit and
-    // shared by both operands; the K position goes in the scalar offset.
+    // ---- direct global -> LDS loads (buffer_load_dwordx4 ... lds): for each operand and
+    // stage, each wave fills 32 rows of that operand's buffer, 8 rows per instruction (lane l
+    // -> row l >> 3, position l & 7 of the swizzled row).  Each operand's descriptor spans
+    // only the rows of this tile that exist, so rows past N or V read as zeros (their results
+    // are never used) and no load can leave the operand.  Lane offsets are 32-bit; the K
+    // position goes in the scalar offset.
     const int64_t h_rows = (a.n_rows - m0) < kBM ? (a.n_rows - m0) : kBM;
     const int64_t w_rows = (a.vocab - n0) < kBN ? (a.vocab - n0) : kBN;
     const __amdgpu_buffer_rsrc_t rh = __builtin_amdgcn_make_buffer_rsrc(
@@ -136,23 +143,29 @@ __global__ __launch_bounds__(kThreads, 1) void fused_lse_kernel(FusedArgs a) {
         const int R = 32 * wave + 8 * i + lr;
         voff[i] = (R * d + ((lp ^ swz(R)) * 8)) * 2;
     }
-    auto issue = [&](int j) {
-        char *st = lds + (j & 1) * kStageB;
+    auto issue = [&](const __amdgpu_buffer_rsrc_t &rsrc, int j, int buf) {
+        char *dst = lds + buf * kBufB;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
+        for (int i = 0; i < 4; ++i)
             __builtin_amdgcn_raw_ptr_buffer_load_lds(
-                rh, LDS_PTR(st + (32 * wave + 8 * i) * kRowB), 16, voff[i], j * kRowB, 0, 0);
-            __builtin_amdgcn_raw_ptr_buffer_load_lds(
-                rw, LDS_PTR(st + kTileB + (32 * wave + 8 * i) * kRowB), 16, voff[i], j * kRowB, 0, 0);
-        }
+                rsrc, LDS_PTR(dst + (32 * wave + 8 * i) * kRowB), 16, voff[i], j * kRowB, 0, 0);
     };
 
     // ---- MFMA fragments: W is the A operand and H the B operand, so lane l's
-    // accumulators hold token j*32 + l%32 and 16 vocabulary entries of it.
+    // accumulators hold token j*32 + l%32 and 16 vocabulary entries of it.  Fragment
+    // addresses are fixed per buffer pair {0,1}, {2,3}, {4}: the buffer's place in its pair
+    // and the 32-row sub-tile go in the read's immediate offset.
     const int fr = lane & 31, fh = lane >> 5;
-    int foff[4];
+    int wb[3][4], hb[3][4];
 #pragma unroll
-    for (int kq = 0; kq < 4; ++kq) foff[kq] = fr * kRowB + (((2 * kq + fh) ^ swz(fr)) * 16);
+    for (int kq = 0; kq < 4; ++kq) {
+        const int f = fr * kRowB + (((2 * kq + fh) ^ swz(fr)) * 16);
+#pragma unroll
+        for (int g = 0; g < 3; ++g) {
+            wb[g][kq] = g * 2 * kBufB + (wv * 128) * kRowB + f;
+            hb[g][kq] = g * 2 * kBufB + (wt * 64) * kRowB + f;
+        }
+    }
     bf16x8 FA[2][4], FB[2][2];
     f32x16 acc[4][2];
 #pragma unroll
@@ -162,29 +175,39 @@ __global__ __launch_bounds__(kThreads, 1) void fused_lse_kernel(FusedArgs a) {
 #pragma unroll
             for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.0f;
 
-    // One 32-wide K step of this wave: fragments from LDS (and, at the first half
-    // of a stage, the loads of the stage after next's slot), then the MFMAs.  The
-    // two groups are one phase apart, so every barrier is met by all eight waves:
-    // group 0 at the end of a memory phase when group 1 ends a compute phase, and
-    // the other way round.  Stage j+1 is loaded into the slot of stage j-1 once both
-    // groups have read stage j-1's fragments, and every wave has its share of stage
-    // j+1 in LDS before the barrier that ends its second phase of stage j.
-    auto phase = [&](int j, int hf) {
-        const char *st = lds + (j & 1) * kStageB;
-        const char *Ws = st + kTileB + (wv * 128) * kRowB;
-        const char *Hs = st + (wt * 64) * kRowB;
+    // One 32-wide K step of this wave (half hf of stage j, whose H and W operands sit in
+    // buffers hbuf and wbuf): fragments from LDS and one operand's loads, then the MFMAs.
+    // The two groups are one phase apart, so every barrier is met by all eight waves: group
+    // 0 at the end of a memory phase when group 1 ends a compute phase, and the other way
+    // round.  The first half-stage loads W(j+1) into the buffer of H(j-1); the second loads
+    // H(j+2) into the buffer of W(j-1) (both read for the last time in stage j-1) and waits
+    // until this wave's shares of H(j+1) and W(j+1) have landed, so stage j+1 is complete in
+    // LDS at the barrier that ends stage j.
+    auto phase = [&](int j, int hf, int hbuf, int wbuf) {
 #pragma unroll
         for (int k2 = 0; k2 < 2; ++k2) {
             const int kq = 2 * hf + k2;
 #pragma unroll
             for (int t = 0; t < 4; ++t)
-                FA[k2][t] = *reinterpret_cast<const bf16x8 *>(Ws + t * 32 * kRowB + foff[kq]);
+                FA[k2][t] = *reinterpret_cast<const bf16x8 *>(
+                    lds + wb[wbuf >> 1][kq] + (wbuf & 1) * kBufB + t * 32 * kRowB);
 #pragma unroll
             for (int t = 0; t < 2; ++t)
-                FB[k2][t] = *reinterpret_cast<const bf16x8 *>(Hs + t * 32 * kRowB + foff[kq]);
+                FB[k2][t] = *reinterpret_cast<const bf16x8 *>(
+                    lds + hb[hbuf >> 1][kq] + (hbuf & 1) * kBufB + t * 32 * kRowB);
         }
-        if (hf == 0 && j >= 1 && j + 1 < ns) issue(j + 1);
-        if (hf == 1) wait_vmem<0>();
+        if (hf == 0) {
+            const int nb = wbuf + 2 >= kBuffers ? wbuf + 2 - kBuffers : wbuf + 2;
+            if (j + 1 < ns) issue(rw, j + 1, nb);
+        } else {
+            const int nb = hbuf + 4 >= kBuffers ? hbuf + 4 - kBuffers : hbuf + 4;
+            if (j + 2 < ns) {
+                issue(rh, j + 2, nb);
+                wait_vmem<4>();
+            } else {
+                wait_vmem<0>();
+            }
+        }
         wait_lds();
         barrier();
 #pragma unroll
@@ -197,19 +220,36 @@ __global__ __launch_bounds__(kThreads, 1) void fused_lse_kernel(FusedArgs a) {
                                                                          acc[i][jj], 0, 0, 0);
         barrier();
     };
-    issue(0);
+    // H(j) lives in buffer 2j mod 5 and W(j) in buffer 2j+1 mod 5; r = j mod 5 is a
+    // compile-time value at every call, so every buffer index is.
+    auto stage = [&](int j, int r) {
+        const int hbuf = (2 * r) % kBuffers, wbuf = (2 * r + 1) % kBuffers;
+        phase(j, 0, hbuf, wbuf);
+        phase(j, 1, hbuf, wbuf);
+    };
+    // prologue: H(0), W(0), H(1) in flight, H(0) and W(0) landed
+    issue(rh, 0, 0);
+    issue(rw, 0, 1);
     if (ns > 1) {
-        issue(1);
-        wait_vmem<8>();  // stage 0 has landed
+        issue(rh, 1, 2);
+        wait_vmem<4>();
     } else {
         wait_vmem<0>();
     }
     barrier();
     if (grp == 1) barrier();  // group 1 runs one phase behind
-    for (int j = 0; j < ns; ++j) {
-        phase(j, 0);
-        phase(j, 1);
+    int j = 0;
+    for (; j + 4 < ns; j += 5) {
+        stage(j, 0);
+        stage(j + 1, 1);
+        stage(j + 2, 2);
+        stage(j + 3, 3);
+        stage(j + 4, 4);
     }
+    if (j < ns) stage(j, 0);  // j is a multiple of 5 here
+    if (j + 1 < ns) stage(j + 1, 1);
+    if (j + 2 < ns) stage(j + 2, 2);
+    if (j + 3 < ns) stage(j + 3, 3);
     if (grp == 0) barrier();  // both groups meet the same number of barriers
 
     // ---- epilogue: per token of this wave, (max, sum exp(z - max)) over its 128 entries ----
