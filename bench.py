@@ -353,6 +353,49 @@ def bench_online(args):
         print(json.dumps(line), flush=True)
 
 
+def bench_gemm_reference(args):
+    """The unfused alternative to the fused projection, for scale: the vendor library's bf16 GEMM
+    (torch.matmul -> hipBLASLt) writing the [N, V] teacher logits, then torch.logsumexp over them,
+    on the fused workload's operands.  A measurement aid only: nothing here is part of the path."""
+    import torch
+
+    from synth import workloads as W
+    from tests import harness as H
+
+    wl = W.make("fused", seed=args.seed)
+    inp = H.device_inputs_fused(wl)
+    h, w_vd = inp["hidden"], inp["w"]
+    w_dv = w_vd.t().contiguous()  # [d, V], contiguous: no transposed view reaches the GEMM
+    del inp
+    stream = torch.cuda.current_stream()
+    torch.cuda.synchronize()
+    reps = max(args.steps // 4, 3)
+    z = torch.matmul(h, w_dv)
+    torch.logsumexp(z, dim=1)
+    torch.cuda.synchronize()
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(reps)]
+    for e in ev:
+        e[0].record(stream)
+        z = torch.matmul(h, w_dv)
+        e[1].record(stream)
+        lse = torch.logsumexp(z, dim=1)
+        e[2].record(stream)
+    torch.cuda.synchronize()
+    mm = stats_ms([(e[0], e[1]) for e in ev])
+    ls = stats_ms([(e[1], e[2]) for e in ev])
+    flops = 2.0 * wl.n_tokens * wl.fused_d * wl.vocab
+    print(json.dumps({
+        "metric": "unfused reference: bf16 GEMM writing the logits, then logsumexp (torch / hipBLASLt)",
+        "value": flops / (mm["mean"] * 1e-3) / 1e12, "unit": "TFLOP/s (GEMM alone)", "n_gpus": 1,
+        "steps": reps, "warmup": 1, "ms_per_step": mm["mean"] + ls["mean"], "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": f"fused operands: h [{wl.n_tokens}, {wl.fused_d}] x W [{wl.fused_d}, "
+                               f"{wl.vocab}] bf16, logits [{wl.n_tokens}, {wl.vocab}] bf16 in HBM",
+                   "global_batch": wl.n_rollouts, "seq_len": wl.n_tokens // wl.n_rollouts,
+                   "parallelism": "single GPU"},
+        "gemm_ms": mm, "logsumexp_ms": ls, "lse_sample": float(lse[0].float().item())}), flush=True)
+
+
 def bench_records(args):
     """Host trajectory record H(x): put a record per task, then plan every task's restart point
     in one call (Sec. 4.2 on the host)."""
@@ -382,7 +425,7 @@ def bench_records(args):
         "put_tasks_per_s_with_binding": n_tasks / put_s}), flush=True)
 
 
-def main():
+def build_parser() -> argparse.ArgumentParser:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
@@ -402,6 +445,9 @@ def main():
                     help="only time the online stop test (stride_stop_step) per call")
     ap.add_argument("--records", action="store_true",
                     help="only time the host trajectory record (put / plan)")
+    ap.add_argument("--gemm-reference", action="store_true",
+                    help="only time the unfused alternative to the fused projection on its operands: "
+                         "torch.matmul (hipBLASLt) writing the logits, then torch.logsumexp")
     ap.add_argument("--read-sweep", action="store_true",
                     help="only measure the streaming read rate against footprint on the "
                          "workload's logits buffers (row pattern and grid-stride order)")
@@ -409,7 +455,11 @@ def main():
                     help="only run a plain elementwise copy (torch.neg on float32) reading and "
                          "writing BYTES each per dispatch, to calibrate the HBM byte counters; keep "
                          "BYTES <= 1 GiB so that torch issues one dispatch per copy")
-    args = ap.parse_args()
+    return ap
+
+
+def main():
+    args = build_parser().parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only: --gpus {args.gpus} is not supported "
               "(the path shards by whole rollouts with no exchange between GPUs)", file=sys.stderr)
@@ -442,6 +492,8 @@ def main():
         return bench_online(args)
     if args.read_sweep:
         return bench_read_sweep(args)
+    if args.gemm_reference:
+        return bench_gemm_reference(args)
     if args.workload == "fused":
         return bench_fused(args)
     wl = W.make(args.workload, seed=args.seed)

@@ -24,3 +24,13 @@ def test_record_store_timing_prints_one_json_line():
     line = json.loads(lines[0])
     assert line["unit"] == "tasks/s" and line["value"] > 0
     assert line["config"]["workload"].startswith("records:")
+
+
+def test_default_workload_is_the_largest_logits_streaming_one():
+    """With no flags the bench measures the long single-turn reasoning batch (8 x 16,384 tokens,
+    79.7 GB of logits), one GPU, and a step count that finishes in seconds."""
+    sys.path.insert(0, ROOT)
+    import bench
+    args = bench.build_parser().parse_args([])
+    assert args.workload == "reasoning" and args.gpus == 1
+    assert 1 <= args.steps <= 100 and args.warmup >= 1
