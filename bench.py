@@ -265,6 +265,19 @@ def bench_fused(args):
     torch.cuda.synchronize()
     k_stats = stats_ms(ev)
     k_ms = k_stats["mean"]
+    # the student stream alone: the same row-scoring kernel over the student's bf16 rows
+    # (scored as the only teacher, so nothing else is read)
+    ls = torch.empty_like(path.logp_t)
+    ev_s = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+            for _ in range(max(args.steps // 2, 3))]
+    for a, b in ev_s:
+        a.record(stream)
+        P.stride_score(inp["layout"], wl.vocab, [inp["student"]], None, inp["ids"], ls, None, None,
+                       tm, path.flags, path.ws)
+        b.record(stream)
+    torch.cuda.synchronize()
+    s_stats = stats_ms(ev_s)
+    s_bytes = wl.n_tokens * (wl.vocab * 2 + 4 + 4)
     flops = 2.0 * wl.n_tokens * wl.fused_d * wl.vocab
     achieved = flops / (k_ms * 1e-3) / 1e12
     log(f"[bench] {args.steps} steps: {ms_step:.3f} ms/step; teacher projection {k_ms:.3f} ms "
@@ -288,6 +301,11 @@ def bench_fused(args):
                      "kernel_ms_min": k_stats["min"],
                      "mfma_busy": measured_mfma_busy(),
                      "flops_per_launch": flops},
+        "student_stream": {"kernel": "score_rows_kernel<bf16> over the student rows alone",
+                           "bytes_per_launch": s_bytes, "ms": s_stats["mean"],
+                           "ms_median": s_stats["median"], "ms_min": s_stats["min"],
+                           "GB/s": s_bytes / (s_stats["mean"] * 1e-3) / 1e9,
+                           "frac_of_hbm_peak": s_bytes / (s_stats["mean"] * 1e-3) / 1e9 / HBM_PEAK_GBS},
     }
     if not args.no_cpu:
         log("[bench] timing the float64 oracle on a bounded sample")

@@ -171,3 +171,41 @@ def test_noalloc_stop_rejects_layouts_past_its_fixed_scratch():
                               stream=0)
     assert ei.value.status == 2
     assert "scratch" in P.library().stride_last_error().decode()
+
+
+def test_last_error_is_per_thread():
+    """Argument errors raised concurrently on several host threads each leave their own message:
+    the library keeps the last error per thread, so a caller never reads another thread's."""
+    import threading
+
+    lay = _layout()
+    x = torch.zeros((10, 16), dtype=torch.float32)
+    ids = torch.zeros(10, dtype=torch.int32)
+    out = _fake(10)
+    tm = torch.zeros(3, dtype=torch.float64)
+    ws = torch.zeros(P.stride_workspace_size(lay, P.STRIDE_UNIT_TOKEN), dtype=torch.uint8)
+    failures = []
+
+    def worker(kind):
+        for _ in range(300):
+            try:
+                if kind == "vocab":
+                    P.stride_score(lay, 0, [x], x, ids, out, out, out, tm, None, ws, stream=0)
+                else:
+                    P.stride_score(lay, 17, [x], x, ids, out, out, out, tm, None, ws, stream=0)
+            except P.stride.StrideError as e:
+                msg = str(e)
+                want = "vocab = 0" if kind == "vocab" else "ld = 16 < vocab = 17"
+                if want not in msg:
+                    failures.append((kind, msg))
+                    return
+            else:
+                failures.append((kind, "no error"))
+                return
+
+    threads = [threading.Thread(target=worker, args=(k,)) for k in ("vocab", "ld") * 4]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join()
+    assert not failures, failures[:3]
