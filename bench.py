@@ -131,6 +131,64 @@ def cpu_baseline(wl, lam, alpha, budget_s: float):
                       f"{t_gen:.1f} s not counted"}
 
 
+def power_under_load(step, seconds: float):
+    """Socket power, graphics clocks and hotspot temperature read with amd-smi (read-only
+    queries) while `step` runs back to back for `seconds`, after the timed region: nothing here
+    is part of the timed numbers.  Samples from the first second of load are dropped."""
+    import shutil
+    import subprocess
+    import threading
+
+    import torch
+
+    exe = shutil.which("amd-smi")
+    if exe is None:
+        return {"error": "amd-smi not found"}
+    samples, stop = [], threading.Event()
+    t_start = time.perf_counter()
+
+    def sampler():
+        while not stop.is_set():
+            t = time.perf_counter() - t_start
+            try:
+                r = subprocess.run([exe, "metric", "-p", "-c", "-t", "--json"], capture_output=True,
+                                   text=True, timeout=20)
+                d = json.loads(r.stdout)
+                g = (d["gpu_data"] if isinstance(d, dict) else d)[0]
+                clk = [v["clk"]["value"] for k, v in g["clock"].items()
+                       if k.startswith("gfx_") and isinstance(v, dict)]
+                samples.append((t, float(g["power"]["socket_power"]["value"]),
+                                sum(clk) / len(clk), float(g["temperature"]["hotspot"]["value"])))
+            except (OSError, ValueError, KeyError, IndexError, TypeError, subprocess.SubprocessError):
+                pass
+            stop.wait(0.2)
+
+    th = threading.Thread(target=sampler, daemon=True)
+    th.start()
+    n = 0
+    while time.perf_counter() - t_start < seconds:
+        step()
+        n += 1
+        if n % 4 == 0:
+            torch.cuda.synchronize()
+    torch.cuda.synchronize()
+    stop.set()
+    th.join(timeout=30)
+    keep = [x for x in samples if x[0] >= 1.0]
+    if not keep:
+        return {"error": "no amd-smi samples under load"}
+
+    def med(i):
+        v = sorted(x[i] for x in keep)
+        return v[len(v) // 2]
+
+    return {"samples": len(keep), "seconds": seconds, "steps": n,
+            "socket_power_W": {"median": med(1), "min": min(x[1] for x in keep),
+                               "max": max(x[1] for x in keep)},
+            "gfx_clock_MHz_median": med(2), "hotspot_C_max": max(x[3] for x in keep),
+            "source": "amd-smi metric -p -c -t (socket power, mean of the gfx clock domains)"}
+
+
 def cpu_baseline_fused(wl, budget_s: float):
     """Float64 oracle on rows of the fused workload (teacher projection in binary64 plus the
     student row), batches of 16 rows until budget_s seconds of oracle compute."""
@@ -278,6 +336,7 @@ def bench_fused(args):
     torch.cuda.synchronize()
     s_stats = stats_ms(ev_s)
     s_bytes = wl.n_tokens * (wl.vocab * 2 + 4 + 4)
+    power = power_under_load(step, args.power) if args.power > 0 else None
     flops = 2.0 * wl.n_tokens * wl.fused_d * wl.vocab
     achieved = flops / (k_ms * 1e-3) / 1e12
     log(f"[bench] {args.steps} steps: {ms_step:.3f} ms/step; teacher projection {k_ms:.3f} ms "
@@ -307,6 +366,8 @@ def bench_fused(args):
                            "GB/s": s_bytes / (s_stats["mean"] * 1e-3) / 1e9,
                            "frac_of_hbm_peak": s_bytes / (s_stats["mean"] * 1e-3) / 1e9 / HBM_PEAK_GBS},
     }
+    if power is not None:
+        res["power"] = power
     if not args.no_cpu:
         log("[bench] timing the float64 oracle on a bounded sample")
         res["cpu_baseline"] = cpu_baseline_fused(wl, args.cpu_seconds)
@@ -455,6 +516,9 @@ def build_parser() -> argparse.ArgumentParser:
                     help="bound on the oracle sample: whole rollouts are added until the oracle "
                          "has computed this long (at least one rollout)")
     ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--power", type=float, default=0.0, metavar="SECONDS",
+                    help="after the timed steps, run the step back to back for SECONDS while "
+                         "sampling socket power, clocks and temperature with amd-smi")
     ap.add_argument("--exact-kl", action="store_true",
                     help="also compute the exact full-vocabulary KL per token (paired kernel)")
     ap.add_argument("--opd-grad", action="store_true",
@@ -660,6 +724,8 @@ def main():
         log(f"[bench] OPD gradient {g_ms:.3f} ms, {kept}/{n_tok} rows retained, "
             f"{res['opd_grad']['achieved_GBs']:.0f} GB/s; read+write reference {c_ms:.3f} ms = "
             f"{copy_gbs:.0f} GB/s")
+    if args.power > 0:
+        res["power"] = power_under_load(step, args.power)
     if not args.no_cpu:
         log("[bench] timing the float64 oracle on a bounded sample")
         res["cpu_baseline"] = cpu_baseline(wl, lam, alpha, args.cpu_seconds)
