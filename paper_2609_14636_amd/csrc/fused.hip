@@ -8,8 +8,10 @@
 //
 // Kernel 1 (MFMA): a 256 x 256 tile of z per workgroup of eight waves, two per
 //   SIMD, each wave holding a 128 (vocabulary) x 64 (token) fp32 accumulator
-//   (8 v_mfma_f32_32x32x16_bf16 tiles, 128 registers).  The waves form two groups
-//   of four (one wave per SIMD) that alternate every 32-wide K step: while one
+//   (32 v_mfma_f32_16x16x32_bf16 tiles, 128 registers).  The 16 x 16 form reads and
+//   writes half as many accumulator registers per product as the 32 x 32 one, and
+//   under this load the chip's power, not its issue rate, sets the pace.  The waves
+//   form two groups of four (one wave per SIMD) that alternate every 32-wide K step: while one
 //   group multiplies from registers, the other reads its next fragments from LDS
 //   and issues loads, then a barrier swaps them (ping-pong), so each SIMD's matrix
 //   unit always has a wave with work.  K = d streams in 64-wide stages through a
@@ -24,9 +26,10 @@
 //   loop: wave-uniform values are scalar and the fragment addresses are fixed per
 //   buffer.  Both operands are K-contiguous, so each MFMA operand is one 16-byte
 //   LDS read.  W is the A operand and H the B operand, so each lane's
-//   accumulators hold 64 of one token's 128 logits and its partner lane (l ^ 32)
-//   the other 64: the epilogue reduces a token to (max, sum of exp(z - max)) with
-//   one exchange and writes it to a partial table [V/128][N] (tokens contiguous).
+//   accumulators hold 32 of one token's 128 logits and the lanes l ^ 16, l ^ 32 and
+//   l ^ 48 the other 96: the epilogue reduces a token to (max, sum of exp(z - max))
+//   with two exchanges and writes it to a partial table [V/128][N] (tokens
+//   contiguous).
 //   Workgroups are numbered so that the 32 resident on one XCD (dispatch is
 //   round-robin over the 8 XCDs) cover a 4 x 8 block of tiles of a 16 x 16
 //   super-tile, and super-tiles advance along V: each XCD's L2 serves every
@@ -45,7 +48,7 @@ namespace stride {
 namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 #define LDS_PTR(p) ((__attribute__((address_space(3))) void *)(p))
@@ -82,9 +85,11 @@ __device__ __forceinline__ float ex2(float x) { return __builtin_amdgcn_exp2f(x)
 // banks (256 B per cycle) and serves a 16-byte-per-lane read in four cycles of 16
 // lanes; on gfx950 a cycle takes four lane quads of one half-wave, quads 0, 3, 5, 6
 // or quads 1, 2, 4, 7 (the quads whose index has even or odd parity; measured with
-// the bank-conflict counter).  Rows are 128 B, so a cycle's 16 rows fall on two bank
-// offsets (row % 2); fragment lane l reads row l % 32, and (r / 2) % 8 takes eight
-// distinct values over the eight rows that share an offset in either kind of cycle.
+// the bank-conflict counter).  Rows are 128 B, so a row's place in the 256-byte bank
+// row is r % 2.  Fragment lane l reads row l % 16 (of a 16-row block) at chunk
+// 4 * hf + l / 16 for the half hf of the stage; over the 16 lanes of either kind of
+// cycle the pairs (r % 2, chunk ^ swz(r)) are all distinct, so every read is free of
+// conflicts.
 __device__ __forceinline__ int swz(int r) { return (r >> 1) & 7; }
 
 // Wait until at most N vector-memory operations of this wave are outstanding.
@@ -143,7 +148,7 @@ __global__ __launch_bounds__(kThreads, 1) void fused_lse_kernel(FusedArgs a) {
         const int R = 32 * wave + 8 * i + lr;
         voff[i] = (R * d + ((lp ^ swz(R)) * 8)) * 2;
     }
-    auto issue = [&](const __amdgpu_buffer_rsrc_t &rsrc, int j, int buf) {
+    auto issue = [&](const __amdgpu_buffer_rsrc_t &rsrc, int j, int buf) __attribute__((always_inline)) {
         char *dst = lds + buf * kBufB;
 #pragma unroll
         for (int i = 0; i < 4; ++i)
@@ -151,29 +156,30 @@ __global__ __launch_bounds__(kThreads, 1) void fused_lse_kernel(FusedArgs a) {
                 rsrc, LDS_PTR(dst + (32 * wave + 8 * i) * kRowB), 16, voff[i], j * kRowB, 0, 0);
     };
 
-    // ---- MFMA fragments: W is the A operand and H the B operand, so lane l's
-    // accumulators hold token j*32 + l%32 and 16 vocabulary entries of it.  Fragment
-    // addresses are fixed per buffer pair {0,1}, {2,3}, {4}: the buffer's place in its pair
-    // and the 32-row sub-tile go in the read's immediate offset.
-    const int fr = lane & 31, fh = lane >> 5;
-    int wb[3][4], hb[3][4];
+    // ---- MFMA fragments: W is the A operand and H the B operand of 16 x 16 x 32 products,
+    // so lane l's accumulators hold token jj*16 + l%16 and 4 vocabulary entries of each
+    // 16-row block.  Lane l reads row l % 16 of a block at chunk 4*hf + l/16; the fragment
+    // addresses are fixed per buffer pair {0,1}, {2,3}, {4} and stage half: the buffer's
+    // place in its pair and the 16-row block go in the read's immediate offset.
+    const int fr = lane & 15, kg = lane >> 4;
+    int wb[3][2], hb[3][2];
 #pragma unroll
-    for (int kq = 0; kq < 4; ++kq) {
-        const int f = fr * kRowB + (((2 * kq + fh) ^ swz(fr)) * 16);
+    for (int hf = 0; hf < 2; ++hf) {
+        const int f = fr * kRowB + (((4 * hf + kg) ^ swz(fr)) * 16);
 #pragma unroll
         for (int g = 0; g < 3; ++g) {
-            wb[g][kq] = g * 2 * kBufB + (wv * 128) * kRowB + f;
-            hb[g][kq] = g * 2 * kBufB + (wt * 64) * kRowB + f;
+            wb[g][hf] = g * 2 * kBufB + (wv * 128) * kRowB + f;
+            hb[g][hf] = g * 2 * kBufB + (wt * 64) * kRowB + f;
         }
     }
-    bf16x8 FA[2][4], FB[2][2];
-    f32x16 acc[4][2];
+    bf16x8 FA[8], FB[4];
+    f32x4 acc[8][4];
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < 8; ++i)
 #pragma unroll
-        for (int j = 0; j < 2; ++j)
+        for (int j = 0; j < 4; ++j)
 #pragma unroll
-            for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.0f;
+            for (int e = 0; e < 4; ++e) acc[i][j][e] = 0.0f;
 
     // One 32-wide K step of this wave (half hf of stage j, whose H and W operands sit in
     // buffers hbuf and wbuf): fragments from LDS and one operand's loads, then the MFMAs.
@@ -183,19 +189,15 @@ __global__ __launch_bounds__(kThreads, 1) void fused_lse_kernel(FusedArgs a) {
     // H(j+2) into the buffer of W(j-1) (both read for the last time in stage j-1) and waits
     // until this wave's shares of H(j+1) and W(j+1) have landed, so stage j+1 is complete in
     // LDS at the barrier that ends stage j.
-    auto phase = [&](int j, int hf, int hbuf, int wbuf) {
+    auto phase = [&](int j, int hf, int hbuf, int wbuf) __attribute__((always_inline)) {
 #pragma unroll
-        for (int k2 = 0; k2 < 2; ++k2) {
-            const int kq = 2 * hf + k2;
+        for (int t = 0; t < 8; ++t)
+            FA[t] = *reinterpret_cast<const bf16x8 *>(lds + wb[wbuf >> 1][hf] + (wbuf & 1) * kBufB +
+                                                      t * 16 * kRowB);
 #pragma unroll
-            for (int t = 0; t < 4; ++t)
-                FA[k2][t] = *reinterpret_cast<const bf16x8 *>(
-                    lds + wb[wbuf >> 1][kq] + (wbuf & 1) * kBufB + t * 32 * kRowB);
-#pragma unroll
-            for (int t = 0; t < 2; ++t)
-                FB[k2][t] = *reinterpret_cast<const bf16x8 *>(
-                    lds + hb[hbuf >> 1][kq] + (hbuf & 1) * kBufB + t * 32 * kRowB);
-        }
+        for (int t = 0; t < 4; ++t)
+            FB[t] = *reinterpret_cast<const bf16x8 *>(lds + hb[hbuf >> 1][hf] + (hbuf & 1) * kBufB +
+                                                      t * 16 * kRowB);
         if (hf == 0) {
             const int nb = wbuf + 2 >= kBuffers ? wbuf + 2 - kBuffers : wbuf + 2;
             if (j + 1 < ns) issue(rw, j + 1, nb);
@@ -211,18 +213,15 @@ __global__ __launch_bounds__(kThreads, 1) void fused_lse_kernel(FusedArgs a) {
         wait_lds();
         barrier();
 #pragma unroll
-        for (int k2 = 0; k2 < 2; ++k2)
+        for (int i = 0; i < 8; ++i)
 #pragma unroll
-            for (int i = 0; i < 4; ++i)
-#pragma unroll
-                for (int jj = 0; jj < 2; ++jj)
-                    acc[i][jj] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(FA[k2][i], FB[k2][jj],
-                                                                         acc[i][jj], 0, 0, 0);
+            for (int jj = 0; jj < 4; ++jj)
+                acc[i][jj] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(FA[i], FB[jj], acc[i][jj], 0, 0, 0);
         barrier();
     };
     // H(j) lives in buffer 2j mod 5 and W(j) in buffer 2j+1 mod 5; r = j mod 5 is a
     // compile-time value at every call, so every buffer index is.
-    auto stage = [&](int j, int r) {
+    auto stage = [&](int j, int r) __attribute__((always_inline)) {
         const int hbuf = (2 * r) % kBuffers, wbuf = (2 * r + 1) % kBuffers;
         phase(j, 0, hbuf, wbuf);
         phase(j, 1, hbuf, wbuf);
@@ -252,41 +251,40 @@ __global__ __launch_bounds__(kThreads, 1) void fused_lse_kernel(FusedArgs a) {
     if (j + 3 < ns) stage(j + 3, 3);
     if (grp == 0) barrier();  // both groups meet the same number of barriers
 
-    // ---- epilogue: per token of this wave, (max, sum exp(z - max)) over its 128 entries ----
-    const int half = lane >> 5;
+    // ---- epilogue: per token of this wave, (max, sum exp(z - max)) over its 128 entries;
+    // lane l holds entries i*16 + 4*(l/16) + e of token jj*16 + l%16, and the lanes l, l^16,
+    // l^32, l^48 that share a token combine theirs with two exchanges ----
+    const int q4 = lane >> 4;
     const int64_t v_base = n0 + wv * 128;
     const int vlim = (int)((a.vocab - v_base) < 128 ? (a.vocab - v_base) : 128);  // valid entries
     const int hidx = tn * 2 + wv;
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
-        float vals[64];
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-#pragma unroll
-            for (int r = 0; r < 16; ++r) vals[i * 16 + r] = acc[i][j][r];
+    for (int jj = 0; jj < 4; ++jj) {
         if (vlim < 128) {
 #pragma unroll
-            for (int i = 0; i < 4; ++i)
+            for (int i = 0; i < 8; ++i)
 #pragma unroll
-                for (int r = 0; r < 16; ++r)
-                    if (i * 32 + (r >> 2) * 8 + half * 4 + (r & 3) >= vlim) vals[i * 16 + r] = -INFINITY;
+                for (int e = 0; e < 4; ++e)
+                    if (i * 16 + q4 * 4 + e >= vlim) acc[i][jj][e] = -INFINITY;
         }
-        float m = vals[0];
+        float m = acc[0][jj][0];
 #pragma unroll
-        for (int e = 1; e < 64; ++e) m = fmaxf(m, vals[e]);
+        for (int x = 1; x < 32; ++x) m = fmaxf(m, acc[x >> 2][jj][x & 3]);
+        m = fmaxf(m, __shfl_xor(m, 16, 64));
         m = fmaxf(m, __shfl_xor(m, 32, 64));
         const float ref = (m == -INFINITY) ? 0.0f : m;
         const float mref = ref * kLog2e;
         float s0 = 0.0f, s1 = 0.0f;
 #pragma unroll
-        for (int e = 0; e < 64; e += 2) {
-            s0 += ex2(__builtin_fmaf(vals[e], kLog2e, -mref));
-            s1 += ex2(__builtin_fmaf(vals[e + 1], kLog2e, -mref));
+        for (int x = 0; x < 32; x += 2) {
+            s0 += ex2(__builtin_fmaf(acc[x >> 2][jj][x & 3], kLog2e, -mref));
+            s1 += ex2(__builtin_fmaf(acc[(x + 1) >> 2][jj][(x + 1) & 3], kLog2e, -mref));
         }
         float sum = s0 + s1;
+        sum += __shfl_xor(sum, 16, 64);
         sum += __shfl_xor(sum, 32, 64);
-        const int64_t row = m0 + wt * 64 + j * 32 + (lane & 31);
-        if (half == 0 && hidx < a.n_half && row < a.n_rows)
+        const int64_t row = m0 + wt * 64 + jj * 16 + (lane & 15);
+        if (q4 == 0 && hidx < a.n_half && row < a.n_rows)
             a.partial[(int64_t)hidx * a.n_rows + row] = make_float2(m, sum);
     }
 }
@@ -381,7 +379,7 @@ __global__ __launch_bounds__(256) void fused_merge_kernel(const float2 *partial,
 
 namespace {
 
-// The projection kernel's dynamic LDS (128 KB) is above the default limit; the limit is
+// The projection kernel's dynamic LDS (160 KB) is above the default limit; the limit is
 // raised once per device, so later calls (and calls under stream capture) make no
 // attribute call.
 hipError_t ensure_lds_limit() {
