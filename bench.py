@@ -354,7 +354,7 @@ def bench_fused(args):
         "roofline": {"bound": "mfma", "achieved": achieved, "peak": MFMA_BF16_PEAK_TFLOPS,
                      "unit": "TFLOP/s", "frac": achieved / MFMA_BF16_PEAK_TFLOPS,
                      "traffic": measured_traffic("fused", FUSED_SRC, "fused_hip_sha256_16"),
-                     "kernel": "fused_lse_kernel (bf16 MFMA 32x32x16); kernel_ms brackets the "
+                     "kernel": "fused_lse_kernel (bf16 MFMA 16x16x32); kernel_ms brackets the "
                                "teacher call (projection + per-row gather + merge)",
                      "kernel_ms": k_ms, "kernel_ms_median": k_stats["median"],
                      "kernel_ms_min": k_stats["min"],
