@@ -209,3 +209,13 @@ def test_last_error_is_per_thread():
     for t in threads:
         t.join()
     assert not failures, failures[:3]
+
+
+def test_c_client_compiles_against_the_header():
+    """The plain C caller (tests/c_client.c) compiles as C11 against include/stride.h alone."""
+    import subprocess
+    src = os.path.join(ROOT, "tests", "c_client.c")
+    r = subprocess.run(["gcc", "-std=c11", "-Wall", "-Werror", "-fsyntax-only",
+                        "-I", os.path.join(ROOT, "include"), "-I", "/opt/rocm/include",
+                        "-D__HIP_PLATFORM_AMD__", src], capture_output=True, text=True)
+    assert r.returncode == 0, r.stderr
