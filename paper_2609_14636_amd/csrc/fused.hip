@@ -173,13 +173,7 @@ __global__ __launch_bounds__(kThreads, 1) void fused_lse_kernel(FusedArgs a) {
         }
     }
     bf16x8 FA[8], FB[4];
-    f32x4 acc[8][4];
-#pragma unroll
-    for (int i = 0; i < 8; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-#pragma unroll
-            for (int e = 0; e < 4; ++e) acc[i][j][e] = 0.0f;
+    f32x4 acc[8][4];  // the first K step's MFMAs start from zero, so no vector moves clear it
 
     // One 32-wide K step of this wave (half hf of stage j, whose H and W operands sit in
     // buffers hbuf and wbuf): fragments from LDS and one operand's loads, then the MFMAs.
@@ -189,7 +183,9 @@ __global__ __launch_bounds__(kThreads, 1) void fused_lse_kernel(FusedArgs a) {
     // H(j+2) into the buffer of W(j-1) (both read for the last time in stage j-1) and waits
     // until this wave's shares of H(j+1) and W(j+1) have landed, so stage j+1 is complete in
     // LDS at the barrier that ends stage j.
-    auto phase = [&](int j, int hf, int hbuf, int wbuf) __attribute__((always_inline)) {
+    // may_start: this call site can be the tile's first K step (stage 0 sits at ring position 0),
+    // whose MFMAs take zero as their accumulator input.
+    auto phase = [&](int j, int hf, int hbuf, int wbuf, bool may_start) __attribute__((always_inline)) {
 #pragma unroll
         for (int t = 0; t < 8; ++t)
             FA[t] = *reinterpret_cast<const bf16x8 *>(lds + wb[wbuf >> 1][hf] + (wbuf & 1) * kBufB +
@@ -212,19 +208,28 @@ __global__ __launch_bounds__(kThreads, 1) void fused_lse_kernel(FusedArgs a) {
         }
         wait_lds();
         barrier();
+        if (may_start && j == 0) {
+            const f32x4 zero = {};
 #pragma unroll
-        for (int i = 0; i < 8; ++i)
+            for (int i = 0; i < 8; ++i)
 #pragma unroll
-            for (int jj = 0; jj < 4; ++jj)
-                acc[i][jj] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(FA[i], FB[jj], acc[i][jj], 0, 0, 0);
+                for (int jj = 0; jj < 4; ++jj)
+                    acc[i][jj] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(FA[i], FB[jj], zero, 0, 0, 0);
+        } else {
+#pragma unroll
+            for (int i = 0; i < 8; ++i)
+#pragma unroll
+                for (int jj = 0; jj < 4; ++jj)
+                    acc[i][jj] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(FA[i], FB[jj], acc[i][jj], 0, 0, 0);
+        }
         barrier();
     };
     // H(j) lives in buffer 2j mod 5 and W(j) in buffer 2j+1 mod 5; r = j mod 5 is a
     // compile-time value at every call, so every buffer index is.
     auto stage = [&](int j, int r) __attribute__((always_inline)) {
         const int hbuf = (2 * r) % kBuffers, wbuf = (2 * r + 1) % kBuffers;
-        phase(j, 0, hbuf, wbuf);
-        phase(j, 1, hbuf, wbuf);
+        phase(j, 0, hbuf, wbuf, r == 0);
+        phase(j, 1, hbuf, wbuf, false);
     };
     // prologue: H(0), W(0), H(1) in flight, H(0) and W(0) landed
     issue(rh, 0, 0);
