@@ -170,6 +170,9 @@ __global__ __launch_bounds__(kThreads, 1) void fused_lse_kernel(FusedArgs a) {
         for (int g = 0; g < 3; ++g) {
             wb[g][hf] = g * 2 * kBufB + (wv * 128) * kRowB + f;
             hb[g][hf] = g * 2 * kBufB + (wt * 64) * kRowB + f;
+            // opaque to the compiler: it would otherwise fold the pair's 64 KB step into the
+            // reads' offsets, overflow their 16-bit immediate and keep a register per read
+            asm volatile("" : "+v"(wb[g][hf]), "+v"(hb[g][hf]));
         }
     }
     bf16x8 FA[8], FB[4];
