@@ -92,9 +92,11 @@ def test_fused_data_errors_flag_only_their_rows():
     say(f"[fused errors] flags {f:#x}, max |d logp_t| on the other {good.size} rows {d:.2e}")
 
 
-def test_fused_wide_hidden_size():
-    """d = 4096 (64 LDS stages of the projection), a partial row tile and a ragged vocabulary."""
-    wl = W.make("fused", seed=4096, scale=dict(R=1, turns=2, tok=40, vocab=1000, d=4096))
+@pytest.mark.parametrize("d", [4096, 65536])
+def test_fused_wide_hidden_size(d):
+    """d = 4096 (64 LDS stages of the projection) and d = 65,536, the largest hidden size the
+    call accepts (1,024 stages), each with a partial row tile and a ragged vocabulary."""
+    wl = W.make("fused", seed=d, scale=dict(R=1, turns=2, tok=40, vocab=1000, d=d))
     sc, _ = H.oracle_fused_scores(wl, np.arange(wl.n_tokens))
     assert sc["flags"] == 0
     per = {0: {k: sc[k] for k in ("logp_t", "logp_s", "kl")}}
@@ -102,10 +104,10 @@ def test_fused_wide_hidden_size():
     ora = {0: (per[0], H.oracle_rollout(wl, 0, per[0], lam, alpha))}
     gpu = H.run_gpu_fused(wl, lam, alpha)
     assert gpu["flags"] == 0, hex(gpu["flags"])
-    d = np.max(np.abs(gpu["logp_t"] - sc["logp_t"]))
-    assert d <= H.TOL_LOGP, d
+    dl = np.max(np.abs(gpu["logp_t"] - sc["logp_t"]))
+    assert dl <= H.TOL_LOGP, dl
     rep = H.compare(wl, gpu, ora, lam, alpha)
-    say(f"[fused d=4096] max |d logp_t| {d:.2e}; {rep}")
+    say(f"[fused d={wl.fused_d}] max |d logp_t| {dl:.2e}; {rep}")
 
 
 def test_restart_pick_with_infinite_values_and_long_records():
