@@ -198,3 +198,75 @@ def test_single_teacher_reads_teacher_zero_whatever_the_domain_ids():
     say(f"[single teacher] R={wl.n_rollouts} N={wl.n_tokens}: domain ids 0..{wl.n_rollouts - 1}")
     for k in ("logp_t", "logp_s", "kl", "turn_mean"):
         assert np.array_equal(outs[0][k].view(np.uint8), outs[1][k].view(np.uint8)), k
+
+
+def test_sixty_four_teachers_and_domains():
+    """The largest domain count the ABI accepts (STRIDE_MAX_DOMAINS = 64): 64 teacher matrices,
+    each routing one rollout (domain ids a permutation of 0..63), and 64 distinct lambda and alpha
+    values chosen from the oracle's own cumulative sums so that rollouts stop at turn 0, at turn 1
+    or not at all, and have 0, 1 or 2 correct turns.  Compared with the oracle row by row."""
+    import torch
+    import paper_2609_14636_amd as P
+    from oracle import oracle as O
+
+    D, K, L, V, ld = 64, 2, 12, 257, 260
+    R, T, N = D, D * K, D * K * L
+    g = np.random.default_rng(6464)
+    dom = ((np.arange(R) * 37) % D).astype(np.int32)
+    rto = (np.arange(R + 1) * K).astype(np.int32)
+    tto = (np.arange(T + 1) * L).astype(np.int64)
+    ids = g.integers(0, V, size=N).astype(np.int32)
+    teachers = [(2.0 * g.standard_normal((N, ld))).astype(np.float32) for _ in range(D)]
+    student = (2.0 * g.standard_normal((N, ld))).astype(np.float32)
+    # oracle: each rollout's rows scored with its own teacher
+    logp_t = np.empty(N)
+    for r in range(R):
+        a, b = r * K * L, (r + 1) * K * L
+        logp_t[a:b] = O.logp_rows(teachers[dom[r]][a:b], ids[a:b], V)[0]
+    logp_s = O.logp_rows(student, ids, V)[0]
+    tm, f = O.turn_mean(tto, logp_t)
+    assert f == 0
+    lam = np.zeros(D)
+    alpha = np.zeros(D)
+    for r in range(R):
+        c0, c1 = tm[2 * r], tm[2 * r] + tm[2 * r + 1]
+        lam[dom[r]] = (c0 + 0.5, 0.5 * (c0 + c1), c1 - 0.5)[r % 3]
+        hi, lo = max(tm[2 * r], tm[2 * r + 1]), min(tm[2 * r], tm[2 * r + 1])
+        alpha[dom[r]] = (hi + 0.5, 0.5 * (hi + lo), lo - 0.5)[r % 4 % 3]
+    uoff = rto.astype(np.int64)
+    cum, stop, _ = O.stop(uoff, tm, lam[dom])
+    rec = np.where(stop >= 0, stop + 1, K).astype(np.int32)
+    ks, k0, km = O.restart(uoff, tm, rec, alpha[dom])
+    assert set(stop.tolist()) == {-1, 0, 1}
+
+    dev = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()  # noqa: E731
+    lay = P.Layout(dev(rto), dev(tto), N, dev(dom))
+    t_dev = [dev(t) for t in teachers]
+    s_dev = dev(student)
+    lt = torch.empty(N, dtype=torch.float32, device="cuda")
+    ls, kl = torch.empty_like(lt), torch.empty_like(lt)
+    tmd = torch.empty(T, dtype=torch.float64, device="cuda")
+    flags = torch.zeros(1, dtype=torch.int32, device="cuda")
+    ws = torch.empty(P.stride_workspace_size(lay, P.STRIDE_UNIT_TURN), dtype=torch.uint8, device="cuda")
+    cumd = torch.empty(T, dtype=torch.float64, device="cuda")
+    stopd = torch.empty(R, dtype=torch.int32, device="cuda")
+    ksd, k0d, kmd = (torch.empty(R, dtype=torch.int32, device="cuda") for _ in range(3))
+    P.stride_score(lay, V, t_dev, s_dev, dev(ids), lt, ls, kl, tmd, flags, ws)
+    P.stride_stop(lay, P.STRIDE_UNIT_TURN, tmd, lam.tolist(), None, cumd, stopd, None, flags, ws)
+    P.stride_restart_turn(lay, P.STRIDE_UNIT_TURN, tmd, stopd, alpha.tolist(), None, ksd, k0d, kmd,
+                          flags)
+    torch.cuda.synchronize()
+    assert int(flags.item()) == 0, hex(int(flags.item()))
+    dlt = np.max(np.abs(lt.cpu().numpy() - logp_t))
+    dls = np.max(np.abs(ls.cpu().numpy() - logp_s))
+    dkl = np.max(np.abs(kl.cpu().numpy() - (logp_s - logp_t)))
+    assert dlt <= H.TOL_LOGP and dls <= H.TOL_LOGP and dkl <= H.TOL_KL, (dlt, dls, dkl)
+    assert np.max(np.abs(tmd.cpu().numpy() - tm)) <= H.TOL_LOGP
+    # thresholds sit at least a quarter of a turn mean away from every value they are tested
+    # against, so stops and picks must match exactly
+    assert np.array_equal(stopd.cpu().numpy(), stop)
+    assert np.array_equal(ksd.cpu().numpy(), ks)
+    assert np.array_equal(k0d.cpu().numpy(), k0)
+    assert np.array_equal(kmd.cpu().numpy(), km)
+    say(f"[64 domains] |d logp_t| {dlt:.2e} |d logp_s| {dls:.2e}; stops "
+        f"{np.bincount(stop + 1).tolist()} (none/0/1), K_max {np.bincount(km).tolist()}")
