@@ -124,3 +124,79 @@ def test_graph_replay_fused_equals_eager():
         for k in want:
             assert np.array_equal(got[k], want[k], equal_nan=True), k
     say("[graph fused] 3 replays equal to eager")
+
+
+def test_graph_replay_of_the_allocation_free_stop_test():
+    """stride_stop_noalloc, the entry point for callers that cannot allocate, captured in a HIP
+    graph: every replay equals stride_stop with a caller workspace on the same inputs bit for bit,
+    with eager calls between the replays that leave other contents in the shared fixed scratch
+    (a smaller layout through stride_stop_noalloc itself) and the values changed in place."""
+    import torch
+    import paper_2609_14636_amd as P
+
+    g = np.random.default_rng(77)
+    dev = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()  # noqa: E731
+
+    def layout(sizes):
+        R = len(sizes)
+        rto = np.arange(R + 1, dtype=np.int32)          # one turn per rollout, token units
+        tto = np.zeros(R + 1, np.int64)
+        tto[1:] = np.cumsum(sizes)
+        return rto, tto
+
+    sizes = np.concatenate([g.integers(1, 3000, size=40), [70000, 2048, 2049]])
+    rto, tto = layout(sizes)
+    N, R = int(tto[-1]), sizes.size
+    dom = g.integers(0, 2, size=R).astype(np.int32)
+    lay = P.Layout(dev(rto), dev(tto), N, dev(dom))
+    vals = dev((-np.abs(g.normal(0.5, 0.5, size=N))).astype(np.float32))
+    start = dev((g.random(R) * sizes * 0.3).astype(np.int32))
+    lam = [-150.0, -900.0]
+    # a second, smaller layout whose eager calls overwrite the fixed scratch between replays
+    sizes2 = g.integers(1, 5000, size=9)
+    rto2, tto2 = layout(sizes2)
+    lay2 = P.Layout(dev(rto2), dev(tto2), int(tto2[-1]), None)
+    vals2 = dev((-np.abs(g.normal(0.3, 0.2, size=int(tto2[-1])))).astype(np.float32))
+
+    def outs(n_units, n_roll):
+        return (torch.empty(n_units, dtype=torch.float64, device="cuda"),
+                torch.empty(n_roll, dtype=torch.int32, device="cuda"),
+                torch.empty(n_roll, dtype=torch.int64, device="cuda"),
+                torch.zeros(1, dtype=torch.int32, device="cuda"))
+
+    got, want, other = outs(N, R), outs(N, R), outs(int(tto2[-1]), sizes2.size)
+    ws = torch.empty(P.stride_workspace_size(lay, P.STRIDE_UNIT_TOKEN), dtype=torch.uint8, device="cuda")
+
+    def captured():
+        P.stride_stop_noalloc(lay, P.STRIDE_UNIT_TOKEN, vals, lam, start, *got)
+
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        captured()  # first call on the device looks up the scratch address, outside the capture
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        captured()
+    torch.cuda.synchronize()
+
+    for rep in range(4):
+        if rep == 2:
+            vals.mul_(1.5)  # the graph reads the values as they are now
+        P.stride_stop_noalloc(lay2, P.STRIDE_UNIT_TOKEN, vals2, [-40.0], None, *other)
+        P.stride_stop(lay, P.STRIDE_UNIT_TOKEN, vals, lam, start, *want, ws)
+        torch.cuda.synchronize()
+        for t in got[:3]:
+            t.fill_(-7)
+        got[3].zero_()
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        assert int(want[3].item()) == 0 and int(got[3].item()) == 0
+        assert np.array_equal(got[0].cpu().numpy().view(np.uint64), want[0].cpu().numpy().view(np.uint64))
+        assert np.array_equal(got[1].cpu().numpy(), want[1].cpu().numpy())
+        assert np.array_equal(got[2].cpu().numpy(), want[2].cpu().numpy())
+    stops = int((want[1] >= 0).sum().item())
+    assert 0 < stops < R
+    say(f"[graph noalloc] 4 replays equal to stride_stop; {stops}/{R} stops")
