@@ -46,6 +46,7 @@ def _per_rollout(wl, sc):
     (1, 3, 100, 4097, 192),     # 300 rows: a partial row tile; V not a multiple of 128
     (2, 2, 150, 257, 64),       # one K block; last 128-column partial has one column
     (1, 2, 40, 100, 64),        # V < 128: one partial 128-column, the tile's other half empty
+    (1, 2, 1, 300, 64),         # two rows in all: one row tile with 254 rows past N
     (1, 2, 33, 256, 320),       # V one whole tile; five K stages, a whole turn of the LDS ring
     (2, 2, 24, 151936, 2048),   # the full hidden size and vocabulary on 96 rows
 ])
