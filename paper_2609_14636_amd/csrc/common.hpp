@@ -10,6 +10,10 @@
 namespace stride {
 
 constexpr int kWave = 64;
+// Threads per workgroup of the one-row-per-wave streaming kernels (the row scoring kernel and
+// the read reference that mirrors it): eight rows per workgroup read about 0.6% faster from
+// HBM than four.
+constexpr int kRowThreads = 512;
 
 // Device-side view of the host's per-domain tables, passed by value.
 struct DomainTable {

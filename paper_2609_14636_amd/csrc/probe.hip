@@ -19,7 +19,7 @@ namespace {
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 constexpr int kUnroll = 8;
 
-__global__ __launch_bounds__(256) void probe_read_kernel(const char *a, const char *b,
+__global__ __launch_bounds__(kRowThreads) void probe_read_kernel(const char *a, const char *b,
                                                          int64_t n_rows, int64_t row_bytes,
                                                          int64_t nvec, uint32_t *sink) {
     const int lane = threadIdx.x & (kWave - 1);
@@ -129,8 +129,9 @@ hipError_t launch_probe_read(const void *a, const void *b, int64_t n_rows, int64
                              int64_t read_bytes, uint32_t *sink, hipStream_t stream) {
     const int64_t items = b ? 2 * n_rows : n_rows;
     if (items == 0) return hipSuccess;
-    const int64_t blocks = (items + 3) / 4;
-    hipLaunchKernelGGL(probe_read_kernel, dim3((unsigned)blocks), dim3(256), 0, stream,
+    constexpr int kRowsPerBlock = kRowThreads / kWave;
+    const int64_t blocks = (items + kRowsPerBlock - 1) / kRowsPerBlock;
+    hipLaunchKernelGGL(probe_read_kernel, dim3((unsigned)blocks), dim3(kRowThreads), 0, stream,
                        static_cast<const char *>(a), static_cast<const char *>(b), n_rows, row_bytes,
                        read_bytes / 16, sink);
     return hipGetLastError();

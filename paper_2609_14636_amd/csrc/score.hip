@@ -3,7 +3,7 @@
 // Eq. (1) (Sec. 3.1): log pi(y_t | y_<t) = x[y_t] - log sum_v exp(x[v]) over the
 // row's V logits.  Each row is read exactly once from HBM.
 //
-// Design (gfx950, wave64): one wavefront per row; a workgroup holds four
+// Design (gfx950, wave64): one wavefront per row; a workgroup holds eight
 // independent rows.  Lanes stream the row with 16-byte non-temporal loads
 // (8 bf16 or 4 fp32 per load, consecutive lanes on consecutive 16-byte words,
 // so one wave instruction moves 1 KiB, fully coalesced).  Each lane keeps a
@@ -102,7 +102,7 @@ struct ScoreArgs {
 };
 
 template <int DT, int U>
-__global__ __launch_bounds__(256) void score_rows_kernel(ScoreArgs a) {
+__global__ __launch_bounds__(kRowThreads) void score_rows_kernel(ScoreArgs a) {
     constexpr int E = Elem<DT>::kPerVec;
     const int lane = threadIdx.x & (kWave - 1);
     const int64_t item = (int64_t)blockIdx.x * (blockDim.x / kWave) + (threadIdx.x / kWave);
@@ -450,13 +450,14 @@ hipError_t launch_score_rows(int32_t dtype, const PtrTable &teachers, int32_t n_
     a.vocab = vocab;
     a.n_teachers = n_teachers;
     const int64_t items = student ? 2 * n_rows : n_rows;
-    const int64_t blocks = (items + 3) / 4;
+    constexpr int kRowsPerBlock = kRowThreads / kWave;
+    const int64_t blocks = (items + kRowsPerBlock - 1) / kRowsPerBlock;
     if (dtype == STRIDE_BF16)
-        hipLaunchKernelGGL((score_rows_kernel<STRIDE_BF16, 8>), dim3((unsigned)blocks), dim3(256), 0,
-                           stream, a);
+        hipLaunchKernelGGL((score_rows_kernel<STRIDE_BF16, 8>), dim3((unsigned)blocks), dim3(kRowThreads),
+                           0, stream, a);
     else
-        hipLaunchKernelGGL((score_rows_kernel<STRIDE_F32, 8>), dim3((unsigned)blocks), dim3(256), 0,
-                           stream, a);
+        hipLaunchKernelGGL((score_rows_kernel<STRIDE_F32, 8>), dim3((unsigned)blocks), dim3(kRowThreads),
+                           0, stream, a);
     return hipGetLastError();
 }
 
