@@ -200,3 +200,46 @@ def test_graph_replay_of_the_allocation_free_stop_test():
     stops = int((want[1] >= 0).sum().item())
     assert 0 < stops < R
     say(f"[graph noalloc] 4 replays equal to stride_stop; {stops}/{R} stops")
+
+
+def test_two_workloads_on_two_streams_equal_sequential_runs():
+    """The calls are asynchronous on the caller's stream and share no state: two different
+    workloads (turn units with a prefix offset and a correctness mask, and token units), each
+    with its own workspace, launched alternately on two non-default streams so that their kernels
+    may overlap, give bit for bit what they give run one after the other on the default stream."""
+    import torch
+    import paper_2609_14636_amd as P
+
+    w1 = W.make("agentic", seed=3031, scale=dict(R=5, turns=6, tok_lo=40, tok_hi=300, vocab=6000))
+    w2 = W.make("reasoning", seed=3032, scale=dict(R=3, tok=5000, vocab=7000))
+    runs = []
+    for wl in (w1, w2):
+        sc = H.oracle_scores(wl, range(wl.n_rollouts), with_student=False)
+        lam, alpha = H.thresholds(wl, sc)
+        runs.append((wl, lam, alpha, H.device_inputs(wl)))
+
+    def go(path, r, stream):
+        wl, lam, alpha, inp = r
+        path.run(wl.vocab, inp["teachers"], inp["student"], inp["ids"], lam, alpha,
+                 start_unit=inp["start"], correct_mask=inp["mask"], stream=stream)
+
+    seq = [P.Path(r[3]["layout"], r[0].unit) for r in runs]
+    for p, r in zip(seq, runs):
+        go(p, r, torch.cuda.current_stream().cuda_stream)
+    torch.cuda.synchronize()
+    want = [{k: np.array(v) for k, v in p.host().items() if v is not None} for p in seq]
+
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    conc = [P.Path(r[3]["layout"], r[0].unit) for r in runs]
+    torch.cuda.synchronize()
+    for rep in range(3):
+        for p, r, s in zip(conc, runs, streams):
+            go(p, r, s.cuda_stream)
+        torch.cuda.synchronize()
+        for p, wnt in zip(conc, want):
+            got = {k: np.array(v) for k, v in p.host().items() if v is not None}
+            for k in wnt:
+                assert np.array_equal(got[k], wnt[k], equal_nan=True), (rep, k)
+    assert int(want[0]["flags"]) == 0 and int(want[1]["flags"]) == 0
+    say(f"[two streams] 3 concurrent runs equal to sequential; stops {want[0]['stop_unit'].tolist()} "
+        f"and {want[1]['stop_unit'].tolist()}")
