@@ -243,3 +243,61 @@ def test_two_workloads_on_two_streams_equal_sequential_runs():
     assert int(want[0]["flags"]) == 0 and int(want[1]["flags"]) == 0
     say(f"[two streams] 3 concurrent runs equal to sequential; stops {want[0]['stop_unit'].tolist()} "
         f"and {want[1]['stop_unit'].tolist()}")
+
+
+def test_two_host_threads_each_on_its_own_stream():
+    """Thread safety of the entry points: two host threads drive two workloads through the
+    library at the same time (ctypes releases the interpreter lock during each call), each on its
+    own stream with its own workspace; every run equals the sequential one bit for bit."""
+    import threading
+
+    import torch
+    import paper_2609_14636_amd as P
+
+    w1 = W.make("multi", seed=3041, scale=dict(R=6, turns=3, tok=200, vocab=5000))
+    w2 = W.make("agentic", seed=3042, scale=dict(R=4, turns=5, tok_lo=30, tok_hi=250, vocab=4096))
+    runs = []
+    for wl in (w1, w2):
+        sc = H.oracle_scores(wl, range(wl.n_rollouts), with_student=False)
+        lam, alpha = H.thresholds(wl, sc)
+        runs.append((wl, lam, alpha, H.device_inputs(wl)))
+
+    def go(path, r, stream):
+        wl, lam, alpha, inp = r
+        path.run(wl.vocab, inp["teachers"], inp["student"], inp["ids"], lam, alpha,
+                 start_unit=inp["start"], correct_mask=inp["mask"], stream=stream)
+
+    want = []
+    for r in runs:
+        p = P.Path(r[3]["layout"], r[0].unit)
+        go(p, r, torch.cuda.current_stream().cuda_stream)
+        torch.cuda.synchronize()
+        want.append({k: np.array(v) for k, v in p.host().items() if v is not None})
+
+    paths = [P.Path(r[3]["layout"], r[0].unit) for r in runs]
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    torch.cuda.synchronize()
+    errors = []
+
+    def worker(i):
+        try:
+            torch.cuda.set_device(0)
+            for _ in range(5):
+                go(paths[i], runs[i], streams[i].cuda_stream)
+                streams[i].synchronize()
+                got = {k: np.array(v) for k, v in paths[i].host().items() if v is not None}
+                for k in want[i]:
+                    if not np.array_equal(got[k], want[i][k], equal_nan=True):
+                        errors.append((i, k))
+                        return
+        except Exception as e:  # noqa: BLE001  (reported below)
+            errors.append((i, repr(e)))
+
+    threads = [threading.Thread(target=worker, args=(i,)) for i in range(2)]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join(timeout=120)
+    assert not any(t.is_alive() for t in threads)
+    assert not errors, errors
+    say("[two threads] 5 runs per thread equal to sequential")
