@@ -1,5 +1,6 @@
 """Edge cases on the GPU: an empty batch through every entry point, data errors in the fused
-projection path, and a fused hidden size past the full-size workload's.
+projection path, a fused hidden size past the full-size workload's, the largest teacher and
+domain count, and a vocabulary of about a million entries.
 
 The empty batch has nothing to compare; every call must succeed, raise no flag and write
 nothing.  The fused error rows must come back NaN with the right flags while every other row
@@ -270,3 +271,31 @@ def test_sixty_four_teachers_and_domains():
     assert np.array_equal(kmd.cpu().numpy(), km)
     say(f"[64 domains] |d logp_t| {dlt:.2e} |d logp_s| {dls:.2e}; stops "
         f"{np.bincount(stop + 1).tolist()} (none/0/1), K_max {np.bincount(km).tolist()}")
+
+
+@pytest.mark.parametrize("dtype", [W.BF16, W.F32])
+def test_million_entry_vocabulary(dtype):
+    """A vocabulary of 2^20 + 5 entries, about seven times the full-size workloads' and with a
+    ragged last 16-byte word: rows of 2 MB (bf16) or 4 MB (fp32), so each lane folds about 2,048
+    words into its running (max, sum).  The whole path against the oracle row by row, then the
+    exact reverse KL of the paired pass."""
+    from tests.test_gpu_parity import _custom, _custom_thresholds
+
+    V = (1 << 20) + 5
+    g = np.random.default_rng(2020 + dtype)
+    lengths = [g.integers(1, 12, size=3) for _ in range(3)]
+    wl = _custom(77 + dtype, V, dtype, lengths)
+    say(f"[vocab 2^20+5] dtype={dtype} R={wl.n_rollouts} N={wl.n_tokens} ld={wl.ld}")
+    sc = H.oracle_scores(wl, range(wl.n_rollouts), exact_kl=True)
+    lam, alpha = _custom_thresholds(wl, sc)
+    ora = {r: (sc[r], H.oracle_rollout(wl, r, sc[r], lam, alpha)) for r in sc}
+    gpu = H.run_gpu(wl, lam, alpha)
+    assert gpu["flags"] == 0, hex(gpu["flags"])
+    rep = H.compare(wl, gpu, ora, lam, alpha)
+    H.assert_invariants(gpu, wl)
+    gk = H.run_gpu(wl, lam, alpha, exact_kl=True)
+    assert gk["flags"] == 0, hex(gk["flags"])
+    want = np.concatenate([sc[r]["kl_full"] for r in range(wl.n_rollouts)])
+    d = np.max(np.abs(gk["kl_full"] - want))
+    assert d <= H.TOL_KL, d
+    say(f"[vocab 2^20+5] {rep}; exact KL max |d| {d:.2e}")

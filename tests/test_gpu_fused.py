@@ -49,6 +49,7 @@ def _per_rollout(wl, sc):
     (1, 2, 1, 300, 64),         # two rows in all: one row tile with 254 rows past N
     (1, 2, 33, 256, 320),       # V one whole tile; five K stages, a whole turn of the LDS ring
     (2, 2, 24, 151936, 2048),   # the full hidden size and vocabulary on 96 rows
+    (1, 2, 16, 1048581, 64),    # 2^20 + 5 entries: 4,097 vocabulary tiles, 8,193 partials per row
 ])
 def test_fused_parity(R, turns, tok, vocab, d):
     wl = W.make("fused", seed=3 + vocab, scale=dict(R=R, turns=turns, tok=tok, vocab=vocab, d=d))

@@ -119,3 +119,16 @@ def test_grad_full_vocab_sampled_rows():
     rng = np.random.default_rng(0)
     rows = np.unique(np.concatenate([rng.integers(0, wl.n_tokens, size=24), [0, wl.n_tokens - 1]]))
     _compare(wl, lam, alpha, scale=1.0 / wl.n_tokens, sample_rows=rows)
+
+
+@pytest.mark.parametrize("dtype", [W.BF16, W.F32])
+def test_grad_million_entry_vocabulary(dtype):
+    """Gradient rows of 2^20 + 5 entries (a ragged last word, padding columns left unwritten),
+    every row and element against the oracle."""
+    g = np.random.default_rng(4040 + dtype)
+    lengths = [g.integers(1, 10, size=3) for _ in range(3)]
+    from tests.test_gpu_parity import _custom, _custom_thresholds
+    wl = _custom(91 + dtype, (1 << 20) + 5, dtype, lengths)
+    sc = H.oracle_scores(wl, range(wl.n_rollouts))
+    lam, alpha = _custom_thresholds(wl, sc)
+    _compare(wl, lam, alpha, scale=1.0 / wl.n_tokens)
