@@ -216,16 +216,11 @@ def test_empty_turn_and_bad_domain_flags():
 
 # ---------------------------------------------------------------- scan and restart at scale
 
-@pytest.mark.parametrize("seed", [0, 1])
-def test_stop_and_restart_many_tiles(seed):
-    """Token-unit scan over 1.2M units: rollouts from 1 to 300k units span many tiles, with K0 and
-    per-domain lambda; inputs are host-made values given to both sides."""
+def _stop_restart_vs_oracle(g, sizes, lam, alpha, tag):
+    """Token-unit stop test and restart pick of one-turn rollouts of the given sizes against the
+    oracle; the unit values, K0 offsets, domains and masks are host-made and given to both sides."""
     import torch
     import paper_2609_14636_amd as P
-    g = np.random.default_rng(seed)
-    sizes = np.concatenate([g.integers(1, 50, size=200), [300000, 2047, 2048, 2049, 250000],
-                            g.integers(1000, 40000, size=20)])
-    g.shuffle(sizes)
     R = sizes.size
     tto = np.zeros(R + 1, np.int64)
     tto[1:] = np.cumsum(sizes)
@@ -233,12 +228,10 @@ def test_stop_and_restart_many_tiles(seed):
     N = int(tto[-1])
     vals = (-np.abs(g.normal(0.5, 0.5, size=N))).astype(np.float32)
     vals[g.random(N) < 0.01] *= 20
-    dom = g.integers(0, 3, size=R).astype(np.int32)
+    dom = g.integers(0, len(lam), size=R).astype(np.int32)
     start = (g.random(R) * sizes * 0.3).astype(np.int32)
     mask = (g.random(N) < 0.999).astype(np.uint8)
-    lam = [-40.0, -400.0, -4000.0]
-    alpha = [-0.9, -1.5, -np.inf]
-    say(f"[scan] R={R} N={N} max rollout {sizes.max()}")
+    say(f"[{tag}] R={R} N={N} max rollout {sizes.max()}")
     # oracle
     uoff = tto.copy()
     cum_o, stop_o, ret_o = H.OP.O.stop(uoff, vals.astype(np.float64), np.array(lam)[dom], start,
@@ -276,7 +269,31 @@ def test_stop_and_restart_many_tiles(seed):
     assert np.array_equal(ks.cpu().numpy()[ok], ks_o[ok])
     assert np.array_equal(km.cpu().numpy()[ok], km_o[ok])
     assert np.array_equal(k0.cpu().numpy()[ok], k0_o[ok])
-    say(f"[scan] max rel cum err {rel.max():.2e}, stops equal {same.sum()}/{R}")
+    say(f"[{tag}] max rel cum err {rel.max():.2e}, stops equal {same.sum()}/{R}, "
+        f"stopped {int((s >= 0).sum())}, k* >= 0 {int((ks.cpu().numpy() >= 0).sum())}")
+    return s
+
+
+@pytest.mark.parametrize("seed", [0, 1])
+def test_stop_and_restart_many_tiles(seed):
+    """Token-unit scan over about a million units: rollouts from 1 to 300k units span many tiles, with K0 and
+    per-domain lambda."""
+    g = np.random.default_rng(seed)
+    sizes = np.concatenate([g.integers(1, 50, size=200), [300000, 2047, 2048, 2049, 250000],
+                            g.integers(1000, 40000, size=20)])
+    g.shuffle(sizes)
+    _stop_restart_vs_oracle(g, sizes, [-40.0, -400.0, -4000.0], [-0.9, -1.5, -np.inf], "scan")
+
+
+def test_stop_and_restart_a_million_short_rollouts():
+    """One million rollouts of one to five units: hundreds of rollout starts in every scan tile,
+    a restart launch of a million workgroups, and 64 domains of lambda and alpha."""
+    g = np.random.default_rng(1000000)
+    sizes = g.integers(1, 6, size=1000000)
+    lam = list(-0.4 - 0.04 * np.arange(64))
+    alpha = list(-0.3 - 0.01 * np.arange(64))
+    s = _stop_restart_vs_oracle(g, sizes, lam, alpha, "short rollouts")
+    assert 0 < int((s >= 0).sum()) < s.size
 
 
 def test_determinism():
