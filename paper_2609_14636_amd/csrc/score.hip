@@ -182,7 +182,11 @@ __global__ __launch_bounds__(kRowThreads) void score_rows_kernel(ScoreArgs a) {
                 xy = __uint_as_float((uint32_t)(reinterpret_cast<const uint16_t *>(p)[y]) << 16);
             else
                 xy = reinterpret_cast<const float *>(p)[y];
-            r = (xy - m) - __builtin_amdgcn_logf(s) * kLn2;
+            // At most 0: the maximum's own term is 1 in exact arithmetic.  Here it is
+            // exp2 of the rounding residual of m * log2(e) (the exponent argument is one fma
+            // against that rounded product), which can sit a few 1e-7 below 1; the clamp
+            // removes only that excess (-inf stays -inf).
+            r = fminf((xy - m) - __builtin_amdgcn_logf(s) * kLn2, 0.0f);
         }
         out[row] = r;
     }
@@ -336,8 +340,8 @@ __global__ __launch_bounds__(256) void score_pairs_kernel(PairArgs a) {
                 xt = reinterpret_cast<const float *>(pt)[y];
                 xs = reinterpret_cast<const float *>(ps)[y];
             }
-            rt = (xt - mt) - lt;
-            rs = (xs - ms) - ls;
+            rt = fminf((xt - mt) - lt, 0.0f);  // at most 0, as in score_rows_kernel
+            rs = fminf((xs - ms) - ls, 0.0f);
         }
         if (bad) raise_flag(a.flags, bad);
         a.logp_t[row] = rt;

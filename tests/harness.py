@@ -290,10 +290,10 @@ def compare(wl: W.Workload, gpu: dict, ora: dict, lam, alpha, rep: Report | None
 def assert_invariants(gpu: dict, wl: W.Workload):
     """Properties that hold at any size: logp <= 0, K0 = max(k*, 0), k* < K_max <= record."""
     lt = gpu["logp_t"]
-    assert np.all(lt[np.isfinite(lt)] <= 1e-6)
+    assert np.all(lt[np.isfinite(lt)] <= 0.0)
     if gpu.get("logp_s") is not None:
         ls = gpu["logp_s"]
-        assert np.all(ls[np.isfinite(ls)] <= 1e-6)
+        assert np.all(ls[np.isfinite(ls)] <= 0.0)
         kl = gpu["kl"]
         both = np.isfinite(lt) & np.isfinite(ls)
         assert np.allclose(kl[both], (ls - lt)[both], atol=1e-6, rtol=0)

@@ -159,6 +159,42 @@ def test_ragged_many_rollouts_token_and_turn_units(unit):
     say(f"[ragged many unit={unit}] {rep}")
 
 
+def test_random_small_layouts():
+    """Eighty random small batches, each through the whole path against the oracle: vocabularies
+    of 1 to 3,000 entries in bf16 or fp32, one to three teachers, turn or token units, empty
+    rollouts, single-token turns, K0 anywhere up to the rollout's end, with and without a mask;
+    every other batch takes the paired pass with the exact KL."""
+    g = np.random.default_rng(777)
+    done = 0
+    for case in range(80):
+        vocab = int(g.choice([1, 2, 7, 8, 9, 63, 64, 65, 511, 512, 513, 3000]))
+        dtype = int(g.choice([W.BF16, W.F32]))
+        R = int(g.integers(1, 12))
+        lengths = [g.integers(1, int(g.integers(2, 60)), size=int(g.integers(0, 6)))
+                   for _ in range(R)]
+        if sum(len(l) for l in lengths) < 2:  # the thresholds need two units
+            lengths[0] = np.array([1, 1])
+        unit = int(g.choice([W.UNIT_TURN, W.UNIT_TOKEN]))
+        wl = _custom(5000 + case, vocab, dtype, lengths, n_teachers=int(g.integers(1, 4)),
+                     unit=unit, start=bool(g.integers(0, 2)), mask=bool(g.integers(0, 2)))
+        exact = case % 2 == 1
+        sc = H.oracle_scores(wl, range(wl.n_rollouts), exact_kl=exact)
+        lam, alpha = _custom_thresholds(wl, sc)
+        ora = {r: (sc[r], H.oracle_rollout(wl, r, sc[r], lam, alpha)) for r in sc}
+        gpu = H.run_gpu(wl, lam, alpha, exact_kl=exact)
+        assert gpu["flags"] == 0, (case, hex(gpu["flags"]))
+        rep = H.compare(wl, gpu, ora, lam, alpha)
+        H.assert_invariants(gpu, wl)
+        if exact:
+            want = np.concatenate([sc[r]["kl_full"] for r in range(wl.n_rollouts)])
+            assert np.max(np.abs(gpu["kl_full"] - want), initial=0.0) <= H.TOL_KL, case
+        done += 1
+        if case % 20 == 19:
+            say(f"[random layouts] case {case}: R={R} N={wl.n_tokens} V={vocab} dtype={dtype} "
+                f"unit={unit} teachers={wl.n_teachers}; {rep}")
+    assert done == 80
+
+
 # ---------------------------------------------------------------- data errors (forced from the host)
 
 def test_data_error_flags():
