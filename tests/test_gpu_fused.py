@@ -50,10 +50,37 @@ def _per_rollout(wl, sc):
     (1, 2, 33, 256, 320),       # V one whole tile; five K stages, a whole turn of the LDS ring
     (2, 2, 24, 151936, 2048),   # the full hidden size and vocabulary on 96 rows
     (1, 2, 16, 1048581, 64),    # 2^20 + 5 entries: 4,097 vocabulary tiles, 8,193 partials per row
+    (1, 2, 5, 1, 128),          # a single vocabulary entry: every log-probability is 0
 ])
 def test_fused_parity(R, turns, tok, vocab, d):
     wl = W.make("fused", seed=3 + vocab, scale=dict(R=R, turns=turns, tok=tok, vocab=vocab, d=d))
     say(f"[fused] N={wl.n_tokens} V={vocab} d={d}")
+    say(f"[fused] {_fused_vs_oracle(wl)}")
+
+
+def test_fused_random_shapes():
+    """Thirty random small shapes against the oracle: 1 to 1,200 rows (partial row tiles),
+    vocabularies of 1 to 5,000 entries (partial 128- and 256-column tiles) and hidden sizes of one
+    to eight K stages."""
+    g = np.random.default_rng(31337)
+    for case in range(30):
+        R, turns = int(g.integers(1, 4)), int(g.integers(1, 5))
+        if R * turns < 2:  # the threshold needs two turns
+            turns = 2
+        tok = int(g.integers(1, 101))
+        vocab = int(g.choice([1, 2, 127, 128, 129, 255, 256, 257])) if g.random() < 0.5 \
+            else int(g.integers(3, 5001))
+        d = 64 * int(g.integers(1, 9))
+        wl = W.make("fused", seed=900 + case,
+                    scale=dict(R=R, turns=turns, tok=tok, vocab=vocab, d=d))
+        rep = _fused_vs_oracle(wl)
+        if case % 10 == 9:
+            say(f"[fused random] case {case}: N={wl.n_tokens} V={vocab} d={d}; {rep}")
+
+
+def _fused_vs_oracle(wl):
+    """Every row of a small fused workload, its turn means, stops and restart picks against the
+    oracle."""
     sc, _ = H.oracle_fused_scores(wl, np.arange(wl.n_tokens))
     assert sc["flags"] == 0
     per = _per_rollout(wl, sc)
@@ -65,7 +92,7 @@ def test_fused_parity(R, turns, tok, vocab, d):
     assert gpu["flags"] == 0, hex(gpu["flags"])
     rep = H.compare(wl, gpu, ora, lam, alpha)
     H.assert_invariants(gpu, wl)
-    say(f"[fused] {rep}")
+    return rep
 
 
 def test_fused_full_size():
