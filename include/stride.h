@@ -358,6 +358,17 @@ stride_status stride_probe_copy(const void *src, void *dst, const uint8_t *row_m
  * STRIDE_ERR_UNSUPPORTED in the product library (libstride.so), which has no delay code. */
 stride_status stride_debug_scan_delay(uint64_t seed, uint32_t one_in, uint32_t sleeps);
 
+/* Test hook of the look-back's bounded wait (not a step of the method).
+ *
+ * In libstride_debug.so, later stride_stop / stride_stop_noalloc calls let a scan tile wait at
+ * most `limit` rounds of s_sleep(1) for each predecessor's descriptor instead of the library's
+ * own bound (2^22 rounds); limit = 0 restores that bound.  With a tiny limit and the delays of
+ * stride_debug_scan_delay, successors give up: the call still completes, raises
+ * STRIDE_FLAG_SPIN_LIMIT and writes NaN to the cumulative values that needed the missing carry,
+ * so the error path can be tested while every wave exits normally.  Process-wide setting.
+ * Returns STRIDE_ERR_UNSUPPORTED in the product library (libstride.so). */
+stride_status stride_debug_scan_spin_limit(uint32_t limit);
+
 /* Message for the last non-OK status returned on this thread ("" if none). */
 const char *stride_last_error(void);
 

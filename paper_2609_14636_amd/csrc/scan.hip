@@ -58,12 +58,16 @@ struct StopArgs {
     uint64_t delay_seed;
     uint32_t delay_one_in;
     uint32_t delay_sleeps;
+    // Test hook, same build only: a look-back wait bound other than kSpinLimit (0: kSpinLimit),
+    // so that the give-up path can be forced from the host.
+    uint32_t spin_limit;
 };
 
 #ifdef STRIDE_SCAN_DELAY_HOOK
 std::atomic<uint64_t> g_delay_seed{0};
 std::atomic<uint32_t> g_delay_one_in{0};
 std::atomic<uint32_t> g_delay_sleeps{0};
+std::atomic<uint32_t> g_spin_limit{0};
 #endif
 
 // unit_off, stop_unit sentinels, descriptor reset, tile counter reset.
@@ -204,14 +208,19 @@ __global__ __launch_bounds__(kScanThreads) void stop_scan_kernel(StopArgs a) {
         const int64_t r0 = s_r0;
         const bool continues = tile > 0 && r0 >= 0 && a.unit_off[r0] < u0;
         if (continues) {
+#ifdef STRIDE_SCAN_DELAY_HOOK
+            const uint32_t limit = a.spin_limit ? a.spin_limit : kSpinLimit;
+#else
+            constexpr uint32_t limit = kSpinLimit;
+#endif
             for (int64_t p = tile - 1; p >= 0; --p) {
                 uint32_t spins = 0;
                 while (__hip_atomic_load(&a.desc[p].status, __ATOMIC_ACQUIRE,
                                          __HIP_MEMORY_SCOPE_AGENT) == 0u) {
-                    if (++spins > kSpinLimit) break;
+                    if (++spins > limit) break;
                     __builtin_amdgcn_s_sleep(1);
                 }
-                if (spins > kSpinLimit) {
+                if (spins > limit) {
                     raise_flag(a.flags, STRIDE_FLAG_SPIN_LIMIT);
                     carry = __builtin_nan("");
                     break;
@@ -412,10 +421,12 @@ hipError_t launch_stop(const stride_layout &L, int32_t unit, const void *values,
     a.delay_seed = g_delay_seed.load();
     a.delay_one_in = g_delay_one_in.load();
     a.delay_sleeps = g_delay_sleeps.load();
+    a.spin_limit = g_spin_limit.load();
 #else
     a.delay_seed = 0;
     a.delay_one_in = 0;
     a.delay_sleeps = 0;
+    a.spin_limit = 0;
 #endif
 
     const int64_t prep_n = (L.n_rollouts + 1 > a.n_tiles) ? L.n_rollouts + 1 : a.n_tiles;
@@ -485,6 +496,16 @@ extern "C" stride_status stride_debug_scan_delay(uint64_t seed, uint32_t one_in,
     (void)seed;
     (void)one_in;
     (void)sleeps;
+    return STRIDE_ERR_UNSUPPORTED;
+#endif
+}
+
+extern "C" stride_status stride_debug_scan_spin_limit(uint32_t limit) {
+#ifdef STRIDE_SCAN_DELAY_HOOK
+    stride::g_spin_limit.store(limit);
+    return STRIDE_OK;
+#else
+    (void)limit;
     return STRIDE_ERR_UNSUPPORTED;
 #endif
 }

@@ -117,6 +117,8 @@ def _load(path: str = LIB_PATH):
     lib.stride_probe_copy.restype = i32
     lib.stride_debug_scan_delay.argtypes = [ctypes.c_uint64, ctypes.c_uint32, ctypes.c_uint32]
     lib.stride_debug_scan_delay.restype = i32
+    lib.stride_debug_scan_spin_limit.argtypes = [ctypes.c_uint32]
+    lib.stride_debug_scan_spin_limit.restype = i32
     lib.stride_last_error.argtypes = []
     lib.stride_last_error.restype = ctypes.c_char_p
     return lib

@@ -7,7 +7,8 @@ find unpublished descriptors and must wait in the look-back.  The waits stay far
 spin limit, so every wave exits normally.  On 1.25 M token units (about 610 tiles, rollouts up
 to 300,000 units long) the cumulative sums must equal the undelayed product library's bit for
 bit, and the stops and restart picks must equal the float64 oracle's.  Stops at the first
-mismatch.
+mismatch.  A second test forces the give-up path: a wait bound of one round makes successors of
+delayed tiles give up, and the call must flag it and mark exactly the values that lack a carry.
 """
 import ctypes
 import sys
@@ -126,4 +127,59 @@ def test_lookback_under_delayed_publication():
             for k, o in (("ks", ks_o), ("k0", k0_o), ("km", km_o)):
                 assert np.array_equal(out[k][same], o[same]), k
     finally:
+        dbg.stride_debug_scan_delay(0, 0, 0)
+
+
+def test_lookback_gives_up_at_a_tiny_spin_limit():
+    """The look-back's give-up path, forced from the host: with every tile delayed before it
+    publishes and a wait bound of one round of s_sleep(1), successors give up.  The calls still
+    complete with STRIDE_FLAG_SPIN_LIMIT, NaN marks exactly the cumulative values that lacked
+    their carry, every finite value equals the normal run bit for bit, rollouts inside one tile
+    are untouched, and the library's own bound restored gives the normal results again."""
+    import torch
+    import paper_2609_14636_amd as P
+    sizes, rto, tto, vals, dom, start, mask = _inputs(1)
+    R, N = sizes.size, int(tto[-1])
+    lam = [-40.0, -400.0, -4000.0]
+    alpha = [-0.9, -1.5, -np.inf]
+    dev = lambda a: torch.from_numpy(a).cuda()
+    lay = P.Layout(dev(rto), dev(tto), N, dev(dom))
+    v, st, mk = dev(vals), dev(start), dev(mask)
+    ws = torch.empty(P.stride_workspace_size(lay, P.STRIDE_UNIT_TOKEN), dtype=torch.uint8,
+                     device="cuda")
+    assert P.library().stride_debug_scan_spin_limit(1) == 2  # the product library has no hook
+    ref = _run(P.library(), lay, v, lam, alpha, st, mk, ws)
+    assert int(ref["flags"][0]) == 0
+
+    dbg = P.stride.debug_library()
+    try:
+        assert dbg.stride_debug_scan_delay(21, 1, 200) == 0
+        assert dbg.stride_debug_scan_spin_limit(1) == 0
+        out = _run(dbg, lay, v, lam, alpha, st, mk, ws)
+        flags = int(out["flags"][0])
+        say(f"[give-up] R={R} N={N}: flags {P.flag_names(flags)}, "
+            f"{int(np.isnan(out['cum']).sum())} cumulative values NaN")
+        assert flags == P.STRIDE_FLAG_SPIN_LIMIT, P.flag_names(flags)
+        nan = np.isnan(out["cum"])
+        assert nan.any()
+        fin = ~nan
+        assert np.array_equal(out["cum"][fin].view(np.uint64), ref["cum"][fin].view(np.uint64))
+        # a NaN needs a carry from an earlier tile: its rollout starts before the NaN's tile
+        unit_r = np.repeat(np.arange(R), sizes)
+        first = tto[:-1][unit_r[nan]]
+        assert np.all(first < (np.nonzero(nan)[0] // 2048) * 2048)
+        # rollouts that start and end in one tile never wait
+        one_tile = (tto[:-1] // 2048) == ((tto[1:] - 1) // 2048)
+        for r in np.nonzero(one_tile & (sizes > 0))[0]:
+            a, b = tto[r], tto[r + 1]
+            assert np.array_equal(out["cum"][a:b].view(np.uint64), ref["cum"][a:b].view(np.uint64))
+            assert out["stop"][r] == ref["stop"][r]
+        # the library's own bound restored: the normal results again, no flag
+        assert dbg.stride_debug_scan_spin_limit(0) == 0
+        again = _run(dbg, lay, v, lam, alpha, st, mk, ws)
+        assert int(again["flags"][0]) == 0
+        for k in ref:
+            assert np.array_equal(again[k].view(np.uint8), ref[k].view(np.uint8)), k
+    finally:
+        dbg.stride_debug_scan_spin_limit(0)
         dbg.stride_debug_scan_delay(0, 0, 0)
