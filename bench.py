@@ -46,6 +46,23 @@ def stats_ms(pairs):
     return {"mean": float(t.mean()), "median": float(np.median(t)), "min": float(t.min())}
 
 
+def check_outputs(out: dict, wl) -> None:
+    """Properties the timed outputs must have at any size (a guard against timing a broken
+    run, not a parity check): finite log-probabilities at most 0, K0 = max(k*, 0),
+    k* < K_max <= the recorded units, and stops inside each rollout."""
+    for k in ("logp_t", "logp_s"):
+        v = out.get(k)
+        if v is not None and not (np.all(np.isfinite(v)) and np.all(v <= 0.0)):
+            raise SystemExit(f"benchmark outputs: {k} not finite or above 0")
+    ks, k0, km, st = out["k_star"], out["k0"], out["k_max"], out["stop_unit"]
+    n_units = np.diff(wl.unit_off())
+    rec = np.where(st >= 0, st + 1, n_units)
+    ok = (np.array_equal(k0, np.maximum(ks, 0)) and np.all((ks == -1) == (km == 0))
+          and np.all(ks < np.maximum(km, 1)) and np.all(km <= rec) and np.all(st < n_units))
+    if not ok:
+        raise SystemExit("benchmark outputs: restart pick or stop outside its bounds")
+
+
 def workload_params(name: str, seed: int):
     with open(PARAMS) as f:
         p = json.load(f)
@@ -240,11 +257,11 @@ def bench_read_sweep(args):
     import torch
 
     import paper_2609_14636_amd as P
+    from synth import device as SD
     from synth import workloads as W
-    from tests import harness as H
 
     wl = W.make(args.workload, seed=args.seed)
-    inp = H.device_inputs(wl)
+    inp = SD.device_inputs(wl)
     t, st = inp["teachers"][0], inp["student"]
     N = wl.n_tokens
     row_bytes = t.stride(0) * t.element_size()
@@ -280,14 +297,14 @@ def bench_fused(args):
     import torch
 
     import paper_2609_14636_amd as P
+    from synth import device as SD
     from synth import workloads as W
-    from tests import harness as H
     from tests import workload_params as WP
 
     wl = W.make("fused", seed=args.seed)
     lam, alpha = WP.fused_thresholds(wl.vocab, wl.fused_d, wl.hidden_sigma, wl.w_sigma)
     log(f"[bench] workload fused seed {args.seed}: N={wl.n_tokens} d={wl.fused_d} V={wl.vocab}")
-    inp = H.device_inputs_fused(wl)
+    inp = SD.device_inputs_fused(wl)
     path = P.Path(inp["layout"], wl.unit, with_student=True, fused_vocab=wl.vocab)
     stream = torch.cuda.current_stream()
     torch.cuda.synchronize()
@@ -308,7 +325,7 @@ def bench_fused(args):
     out = path.host()
     if out["flags"] != 0:
         raise SystemExit(f"device flags {out['flags']:#x} on the benchmark workload")
-    H.assert_invariants(out, wl)
+    check_outputs(out, wl)
     # the dominant kernel alone: teacher-only calls (projection + LSE, plus the
     # per-row gather and merge kernels, <1% of the time)
     lt = torch.empty_like(path.logp_t)
@@ -432,17 +449,94 @@ def bench_online(args):
         print(json.dumps(line), flush=True)
 
 
+def bench_graph(args):
+    """Eager calls against HIP-graph replay of the same step (score -> stop -> restart) on small
+    batches, where the step is six short kernels and their launches dominate: the library
+    allocates, synchronises and memsets nothing, so the step is captured once and replayed with
+    one launch.  A measurement aid; the headline step is timed with eager calls."""
+    import torch
+
+    import paper_2609_14636_amd as P
+    from synth import device as SD
+    from synth import workloads as W
+
+    stream = torch.cuda.current_stream()
+    calls = max(args.steps, 1) * 10
+    lines = []
+    for R, tok in ((8, 8), (16, 64), (64, 256)):
+        wl = W.make("reasoning", seed=args.seed, scale=dict(R=R, tok=tok))
+        inp = SD.device_inputs(wl)
+        lam, alpha = [-0.5 * tok * math.log(wl.vocab)], [-math.inf]
+        paths = [P.Path(inp["layout"], wl.unit) for _ in range(2)]
+
+        def step(path):
+            path.run(wl.vocab, inp["teachers"], inp["student"], inp["ids"], lam, alpha,
+                     start_unit=inp["start"], correct_mask=inp["mask"])
+
+        eager, graphed = paths
+        side = torch.cuda.Stream()
+        side.wait_stream(stream)
+        with torch.cuda.stream(side):
+            step(graphed)  # warm-up outside the capture
+        stream.wait_stream(side)
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            step(graphed)
+        torch.cuda.synchronize()
+        for _ in range(args.warmup):
+            step(eager)
+            g.replay()
+        torch.cuda.synchronize()
+        times, issue = {}, {}
+        for name, fn in (("eager", lambda: step(eager)), ("graph", g.replay)):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            torch.cuda.synchronize()
+            e0.record(stream)
+            t0 = time.perf_counter()
+            for _ in range(calls):
+                fn()
+            issue[name] = (time.perf_counter() - t0) * 1e6 / calls  # host time to issue a step
+            e1.record(stream)
+            torch.cuda.synchronize()
+            times[name] = e0.elapsed_time(e1) * 1e3 / calls
+        a, b = eager.host(), graphed.host()
+        if a["flags"] or b["flags"]:
+            raise SystemExit(f"device flags {a['flags']:#x} / {b['flags']:#x}")
+        for k in a:
+            if a[k] is not None and not np.array_equal(np.asarray(a[k]), np.asarray(b[k])):
+                raise SystemExit(f"graph replay differs from eager calls in {k}")
+        check_outputs(a, wl)
+        log(f"[bench] graph R={R} tok={tok}: eager {times['eager']:.1f} us/step "
+            f"(host issue {issue['eager']:.1f}), graph {times['graph']:.1f} us/step "
+            f"(host issue {issue['graph']:.1f})")
+        lines.append({
+            "metric": "step latency with HIP graph replay (score+stop+restart), 1 MI355X",
+            "value": times["graph"], "unit": "us/step", "n_gpus": 1, "steps": calls,
+            "warmup": args.warmup, "ms_per_step": times["graph"] * 1e-3,
+            "higher_is_better": False, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+            "data": "synthetic",
+            "config": {"workload": f"reasoning-shaped: {R} rollouts x {tok} tokens "
+                                   f"({wl.n_tokens} rows, V={wl.vocab}), token units",
+                       "global_batch": R, "seq_len": tok, "parallelism": "single GPU"},
+            "eager_us_per_step": times["eager"],
+            "host_issue_us_per_step": {"eager": issue["eager"], "graph": issue["graph"]},
+            "graph_speedup": times["eager"] / times["graph"]})
+    for line in lines:
+        print(json.dumps(line), flush=True)
+
+
 def bench_gemm_reference(args):
     """The unfused alternative to the fused projection, for scale: the vendor library's bf16 GEMM
     (torch.matmul -> hipBLASLt) writing the [N, V] teacher logits, then torch.logsumexp over them,
     on the fused workload's operands.  A measurement aid only: nothing here is part of the path."""
     import torch
 
+    from synth import device as SD
     from synth import workloads as W
-    from tests import harness as H
 
     wl = W.make("fused", seed=args.seed)
-    inp = H.device_inputs_fused(wl)
+    inp = SD.device_inputs_fused(wl)
     h, w_vd = inp["hidden"], inp["w"]
     w_dv = w_vd.t().contiguous()  # [d, V], contiguous: no transposed view reaches the GEMM
     del inp
@@ -525,6 +619,8 @@ def build_parser() -> argparse.ArgumentParser:
                     help="also run the OPD loss gradient (stride_opd_grad) in each step")
     ap.add_argument("--online", action="store_true",
                     help="only time the online stop test (stride_stop_step) per call")
+    ap.add_argument("--graph", action="store_true",
+                    help="only time small steps as eager calls against HIP graph replay")
     ap.add_argument("--records", action="store_true",
                     help="only time the host trajectory record (put / plan)")
     ap.add_argument("--gemm-reference", action="store_true",
@@ -566,12 +662,14 @@ def main():
         return bench_records(args)
 
     import paper_2609_14636_amd as P
+    from synth import device as SD
     from synth import workloads as W
-    from tests import harness as H
 
     torch.cuda.set_device(0)
     if args.online:
         return bench_online(args)
+    if args.graph:
+        return bench_graph(args)
     if args.read_sweep:
         return bench_read_sweep(args)
     if args.gemm_reference:
@@ -582,7 +680,7 @@ def main():
     lam, alpha = workload_params(args.workload, args.seed)
     log(f"[bench] workload {args.workload} seed {args.seed}: R={wl.n_rollouts} T={wl.n_turns} "
         f"N={wl.n_tokens} V={wl.vocab}; generating {2 * wl.logits_bytes() / 1e9:.1f} GB on device")
-    inp = H.device_inputs(wl)
+    inp = SD.device_inputs(wl)
     path = P.Path(inp["layout"], wl.unit, with_student=True, exact_kl=args.exact_kl)
     stream = torch.cuda.current_stream()
     torch.cuda.synchronize()
@@ -637,7 +735,7 @@ def main():
     out = path.host()
     if out["flags"] != 0:
         raise SystemExit(f"device flags {out['flags']:#x} on the benchmark workload")
-    H.assert_invariants(out, wl)
+    check_outputs(out, wl)
     log(f"[bench] {args.steps} steps: {ms_step:.3f} ms/step (device: median "
         f"{step_stats['median']:.3f}, min {step_stats['min']:.3f}), scoring mean {score_ms:.3f} "
         f"median {k_stats['median']:.3f} min {k_stats['min']:.3f} ms; "
