@@ -4,9 +4,11 @@
 // row's V logits.  Each row is read exactly once from HBM.
 //
 // Design (gfx950, wave64): one wavefront per row; a workgroup holds eight
-// independent rows.  Lanes stream the row with 16-byte non-temporal loads
-// (8 bf16 or 4 fp32 per load, consecutive lanes on consecutive 16-byte words,
-// so one wave instruction moves 1 KiB, fully coalesced).  Each lane keeps a
+// independent rows (small batches instead share each row among the eight
+// wavefronts of a workgroup: score_rows_split_kernel).  Lanes stream the row
+// with 16-byte non-temporal loads (8 bf16 or 4 fp32 per load, consecutive
+// lanes on consecutive 16-byte words, so one wave instruction moves 1 KiB,
+// fully coalesced).  Each lane keeps a
 // running (max m, sum s) in fp32 registers and rescales once per chunk of
 // U loads, not once per element (online normaliser, Milakov and Gimelshein
 // 2018).  Per element the work is: unpack (shift or mask), max, one fma into
@@ -21,6 +23,12 @@ namespace {
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.69314718055994531f;
 constexpr uint8_t kBadDomain = 0xFF;
+// Row items (teacher and student rows) below which each row gets a workgroup of kSplitWaves
+// wavefronts instead of one wavefront.  Measured on V = 151,936 bf16 rows: the shared rows read
+// as fast or faster up to 16,384 items (64 rows: 14 us against 61 us) and 1-2% slower from
+// 32,768 items on, where one wavefront per row already fills the chip.
+constexpr int kSplitWaves = 8;
+constexpr int64_t kSplitBelow = 16384;
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
@@ -101,6 +109,46 @@ struct ScoreArgs {
     int32_t n_teachers;
 };
 
+// Merge the 64 lane states of a wavefront with a fixed butterfly of cross-lane shuffles (every
+// lane ends with the same result, so it does not depend on timing).
+__device__ __forceinline__ void wave_merge(float &m, float &s) {
+#pragma unroll
+    for (int off = kWave / 2; off > 0; off >>= 1) {
+        const float m2 = __shfl_xor(m, off, kWave);
+        const float s2 = __shfl_xor(s, off, kWave);
+        merge(m, s, m2, s2);
+    }
+}
+
+// The row's result from its (max, sum): log pi(y) = x_y - m - log s, NaN and a flag for a
+// non-finite row or a token id outside [0, V).
+template <int DT>
+__device__ __forceinline__ void write_row(const ScoreArgs &a, int64_t row, const u32x4 *p, float m,
+                                          float s, float *out) {
+    const int32_t y = a.ids[row];
+    float r;
+    uint32_t bad = 0;
+    const bool finite = (m > -INFINITY) && (m < INFINITY) && (s > 0.0f) && (s < INFINITY);
+    if (!finite) bad |= STRIDE_FLAG_NONFINITE;
+    if (y < 0 || y >= a.vocab) bad |= STRIDE_FLAG_TOKEN_OOB;
+    if (bad) {
+        r = __builtin_nanf("");
+        raise_flag(a.flags, bad);
+    } else {
+        float xy;
+        if (DT == STRIDE_BF16)
+            xy = __uint_as_float((uint32_t)(reinterpret_cast<const uint16_t *>(p)[y]) << 16);
+        else
+            xy = reinterpret_cast<const float *>(p)[y];
+        // At most 0: the maximum's own term is 1 in exact arithmetic.  Here it is exp2 of the
+        // rounding residual of m * log2(e) (the exponent argument is one fma against that
+        // rounded product), which can sit a few 1e-7 below 1; the clamp removes only that
+        // excess (-inf stays -inf).
+        r = fminf((xy - m) - __builtin_amdgcn_logf(s) * kLn2, 0.0f);
+    }
+    out[row] = r;
+}
+
 template <int DT, int U>
 __global__ __launch_bounds__(kRowThreads) void score_rows_kernel(ScoreArgs a) {
     constexpr int E = Elem<DT>::kPerVec;
@@ -160,35 +208,84 @@ __global__ __launch_bounds__(kRowThreads) void score_rows_kernel(ScoreArgs a) {
         fold<E>(m, s0, s1, x);
     }
     float s = s0 + s1;
-#pragma unroll
-    for (int off = kWave / 2; off > 0; off >>= 1) {
-        const float m2 = __shfl_xor(m, off, kWave);
-        const float s2 = __shfl_xor(s, off, kWave);
-        merge(m, s, m2, s2);
-    }
-    if (lane == 0) {
-        const int32_t y = a.ids[row];
-        float r;
-        uint32_t bad = 0;
-        const bool finite = (m > -INFINITY) && (m < INFINITY) && (s > 0.0f) && (s < INFINITY);
-        if (!finite) bad |= STRIDE_FLAG_NONFINITE;
-        if (y < 0 || y >= a.vocab) bad |= STRIDE_FLAG_TOKEN_OOB;
-        if (bad) {
-            r = __builtin_nanf("");
-            raise_flag(a.flags, bad);
-        } else {
-            float xy;
-            if (DT == STRIDE_BF16)
-                xy = __uint_as_float((uint32_t)(reinterpret_cast<const uint16_t *>(p)[y]) << 16);
-            else
-                xy = reinterpret_cast<const float *>(p)[y];
-            // At most 0: the maximum's own term is 1 in exact arithmetic.  Here it is
-            // exp2 of the rounding residual of m * log2(e) (the exponent argument is one fma
-            // against that rounded product), which can sit a few 1e-7 below 1; the clamp
-            // removes only that excess (-inf stays -inf).
-            r = fminf((xy - m) - __builtin_amdgcn_logf(s) * kLn2, 0.0f);
+    wave_merge(m, s);
+    if (lane == 0) write_row<DT>(a, row, p, m, s, out);
+}
+
+// Batches too small to fill the chip with one wavefront per row (the online setting scores a
+// few hundred rows per call): a workgroup of kSplitWaves wavefronts shares each row.  Wave w
+// folds the row's U-load chunks w, w + kSplitWaves, ... and every kSplitWaves-th of the words
+// after the last whole chunk; the waves' (max, sum) states are merged in wave order through
+// LDS, so the result does not depend on timing (it differs from score_rows_kernel's only in
+// the order of rounding).
+template <int DT, int U>
+__global__ __launch_bounds__(kSplitWaves *kWave) void score_rows_split_kernel(ScoreArgs a) {
+    constexpr int E = Elem<DT>::kPerVec;
+    __shared__ float s_m[kSplitWaves], s_s[kSplitWaves];
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wave = threadIdx.x / kWave;
+    const int64_t item = blockIdx.x;  // one workgroup per item: the grid has exactly n_items
+    const bool two = a.student != nullptr;
+    const bool is_student = two && (item & 1);
+    const int64_t row = two ? (item >> 1) : item;
+    float *out = is_student ? a.logp_s : a.logp_t;
+
+    const void *base;
+    if (is_student) {
+        base = a.student;
+    } else {
+        const int d = a.row_dom ? (int)a.row_dom[row] : 0;
+        if (d >= a.n_teachers) {  // the same for the whole workgroup: it leaves before any barrier
+            if (threadIdx.x == 0) out[row] = __builtin_nanf("");
+            return;
         }
-        out[row] = r;
+        base = a.teachers.p[d];
+    }
+    const u32x4 *p = reinterpret_cast<const u32x4 *>(static_cast<const char *>(base) +
+                                                     row * a.ld * Elem<DT>::kSize);
+    const int64_t nvec = a.vocab / E;
+    const int tail = a.vocab % E;
+    constexpr int64_t kStep = (int64_t)U * kWave;
+    const int64_t nfull = nvec / kStep;  // whole U-load chunks
+
+    float m = -INFINITY, s0 = 0.0f, s1 = 0.0f;
+    for (int64_t c = wave; c < nfull; c += kSplitWaves) {
+        const int64_t k = c * kStep;
+        u32x4 v[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) v[u] = __builtin_nontemporal_load(p + k + u * kWave + lane);
+        float x[U * E];
+#pragma unroll
+        for (int u = 0; u < U; ++u) unpack<DT>(v[u], x + u * E);
+        fold<U * E>(m, s0, s1, x);
+    }
+    for (int64_t k = nfull * kStep + (int64_t)wave * kWave; k < nvec; k += (int64_t)kSplitWaves * kWave) {
+        if (k + lane < nvec) {
+            u32x4 v = __builtin_nontemporal_load(p + k + lane);
+            float x[E];
+            unpack<DT>(v, x);
+            fold<E>(m, s0, s1, x);
+        }
+    }
+    if (tail && wave == 0 && lane == 0) {
+        u32x4 v = p[nvec];
+        float x[E];
+        unpack<DT>(v, x);
+#pragma unroll
+        for (int j = 0; j < E; ++j)
+            if (j >= tail) x[j] = -INFINITY;
+        fold<E>(m, s0, s1, x);
+    }
+    float s = s0 + s1;
+    wave_merge(m, s);
+    if (lane == 0) {
+        s_m[wave] = m;
+        s_s[wave] = s;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {  // wave 0's state, then waves 1, 2, ... in order
+        for (int w = 1; w < kSplitWaves; ++w) merge(m, s, s_m[w], s_s[w]);
+        write_row<DT>(a, row, p, m, s, out);
     }
 }
 
@@ -454,6 +551,15 @@ hipError_t launch_score_rows(int32_t dtype, const PtrTable &teachers, int32_t n_
     a.vocab = vocab;
     a.n_teachers = n_teachers;
     const int64_t items = student ? 2 * n_rows : n_rows;
+    if (items < kSplitBelow) {
+        if (dtype == STRIDE_BF16)
+            hipLaunchKernelGGL((score_rows_split_kernel<STRIDE_BF16, 8>), dim3((unsigned)items),
+                               dim3(kSplitWaves * kWave), 0, stream, a);
+        else
+            hipLaunchKernelGGL((score_rows_split_kernel<STRIDE_F32, 8>), dim3((unsigned)items),
+                               dim3(kSplitWaves * kWave), 0, stream, a);
+        return hipGetLastError();
+    }
     constexpr int kRowsPerBlock = kRowThreads / kWave;
     const int64_t blocks = (items + kRowsPerBlock - 1) / kRowsPerBlock;
     if (dtype == STRIDE_BF16)

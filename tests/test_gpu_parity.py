@@ -332,6 +332,22 @@ def test_stop_and_restart_a_million_short_rollouts():
     assert 0 < int((s >= 0).sum()) < s.size
 
 
+@pytest.mark.parametrize("n_rows,with_student", [(8191, True), (8192, True), (16383, False),
+                                                  (16384, False)])
+def test_either_side_of_the_shared_row_threshold(n_rows, with_student):
+    """Batches of fewer than 16,384 row items (teacher plus student rows) share each row among the
+    eight wavefronts of a workgroup; larger ones take one wavefront per row.  Both sides of the
+    threshold against the oracle on every row, and the shared form run twice is bit-identical."""
+    wl = W.make("reasoning", seed=17, scale=dict(R=1, tok=n_rows, vocab=4099))
+    gpu, _, lam, alpha, _ = _parity(wl, with_student=with_student)
+    items = n_rows * (2 if with_student else 1)
+    if items < 16384:
+        again = H.run_gpu(wl, lam, alpha, with_student=with_student)
+        for k in ("logp_t", "logp_s", "kl", "turn_mean", "cum", "stop_unit", "k_star"):
+            if gpu.get(k) is not None:
+                assert np.array_equal(gpu[k].view(np.uint8), again[k].view(np.uint8)), k
+
+
 def test_determinism():
     import torch
     wl = W.make("reasoning", seed=5, scale=dict(R=3, tok=3000, vocab=4096))
