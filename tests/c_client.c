@@ -3,7 +3,7 @@
  * files, outputs written to files.  No Python and no torch on this side of the boundary: device
  * memory comes from hipMalloc, and every call goes through the declarations in stride.h.
  *
- * usage: c_client DIR
+ * usage: c_client DIR [--graph]
  *   DIR/meta.txt      "R T N V n_dom unit has_start has_mask has_domain"
  *   DIR/rto.i32       [R+1] rollout -> turn offsets      DIR/tto.i64   [T+1] turn -> row offsets
  *   DIR/teacher.bf16  [N][V] teacher logits (bf16 bits)  DIR/student.bf16 [N][V]
@@ -12,6 +12,9 @@
  *   DIR/domain.i32    [R] (has_domain)
  * writes DIR/out_<name> for logp_t, logp_s, kl (f32 [N]), turn_mean (f64 [T]), cum (f64 [U]),
  * stop, k_star, k0, k_max (i32 [R]), retained (i64 [R]) and flags (u32).
+ * With --graph the same three calls are then captured into a HIP graph on the stream
+ * (hipStreamBeginCapture / hipStreamEndCapture), the outputs are overwritten with a sentinel,
+ * and the graph is replayed three times; every output must equal the eager run's bit for bit.
  */
 #include <stdio.h>
 #include <stdlib.h>
@@ -76,8 +79,17 @@ static void *to_host(const void *d, size_t bytes) {
     return h;
 }
 
+/* device buffer equal, byte for byte, to a host copy */
+static int same_as(const void *d, const void *h, size_t bytes) {
+    void *x = to_host(d, bytes);
+    const int eq = bytes == 0 || memcmp(x, h, bytes) == 0;
+    free(x);
+    return eq;
+}
+
 int main(int argc, char **argv) {
-    if (argc != 2) die("usage", "c_client DIR");
+    const int graph = argc == 3 && strcmp(argv[2], "--graph") == 0;
+    if (argc != 2 && !graph) die("usage", "c_client DIR [--graph]");
     g_dir = argv[1];
     int R, T, V, n_dom, unit, has_start, has_mask, has_domain;
     long long N;
@@ -146,29 +158,61 @@ int main(int argc, char **argv) {
     hip_ok(hipStreamCreate(&stream), "hipStreamCreate");
 
     const void *teachers[1] = {d_teacher};
-    stride_ok(stride_score(&L, V, ld, STRIDE_BF16, 1, teachers, d_student, d_ids, d_logp_t, d_logp_s,
-                           d_kl, NULL, d_turn_mean, d_flags, d_ws, ws_bytes, stream),
-              "stride_score");
     const void *values = unit == STRIDE_UNIT_TURN ? (const void *)d_turn_mean : (const void *)d_logp_t;
-    stride_ok(stride_stop(&L, unit, values, lambda, n_dom, d_start, d_cum, d_stop, d_retained, d_flags,
-                          d_ws, ws_bytes, stream),
-              "stride_stop");
-    stride_ok(stride_restart_turn(&L, unit, values, d_stop, alpha, n_dom, d_mask, d_kstar, d_k0, d_kmax,
-                                  d_flags, stream),
-              "stride_restart_turn");
+    /* score -> stop -> restart, issued on the stream without waiting */
+#define STEP()                                                                                     \
+    do {                                                                                           \
+        stride_ok(stride_score(&L, V, ld, STRIDE_BF16, 1, teachers, d_student, d_ids, d_logp_t,   \
+                               d_logp_s, d_kl, NULL, d_turn_mean, d_flags, d_ws, ws_bytes, stream), \
+                  "stride_score");                                                                 \
+        stride_ok(stride_stop(&L, unit, values, lambda, n_dom, d_start, d_cum, d_stop, d_retained, \
+                              d_flags, d_ws, ws_bytes, stream),                                    \
+                  "stride_stop");                                                                  \
+        stride_ok(stride_restart_turn(&L, unit, values, d_stop, alpha, n_dom, d_mask, d_kstar,     \
+                                      d_k0, d_kmax, d_flags, stream),                              \
+                  "stride_restart_turn");                                                          \
+    } while (0)
+    STEP();
     hip_ok(hipStreamSynchronize(stream), "hipStreamSynchronize");
 
-    write_file("logp_t", to_host(d_logp_t, sizeof(float) * N), sizeof(float) * N);
-    write_file("logp_s", to_host(d_logp_s, sizeof(float) * N), sizeof(float) * N);
-    write_file("kl", to_host(d_kl, sizeof(float) * N), sizeof(float) * N);
-    write_file("turn_mean", to_host(d_turn_mean, sizeof(double) * T), sizeof(double) * T);
-    write_file("cum", to_host(d_cum, sizeof(double) * U), sizeof(double) * U);
-    write_file("stop", to_host(d_stop, sizeof(int32_t) * R), sizeof(int32_t) * R);
-    write_file("retained", to_host(d_retained, sizeof(int64_t) * R), sizeof(int64_t) * R);
-    write_file("k_star", to_host(d_kstar, sizeof(int32_t) * R), sizeof(int32_t) * R);
-    write_file("k0", to_host(d_k0, sizeof(int32_t) * R), sizeof(int32_t) * R);
-    write_file("k_max", to_host(d_kmax, sizeof(int32_t) * R), sizeof(int32_t) * R);
-    write_file("flags", to_host(d_flags, sizeof(uint32_t)), sizeof(uint32_t));
+    struct { const char *name; void *dev; size_t bytes; void *host; } out[] = {
+        {"logp_t", d_logp_t, sizeof(float) * N, NULL},     {"logp_s", d_logp_s, sizeof(float) * N, NULL},
+        {"kl", d_kl, sizeof(float) * N, NULL},             {"turn_mean", d_turn_mean, sizeof(double) * T, NULL},
+        {"cum", d_cum, sizeof(double) * U, NULL},          {"stop", d_stop, sizeof(int32_t) * R, NULL},
+        {"retained", d_retained, sizeof(int64_t) * R, NULL}, {"k_star", d_kstar, sizeof(int32_t) * R, NULL},
+        {"k0", d_k0, sizeof(int32_t) * R, NULL},           {"k_max", d_kmax, sizeof(int32_t) * R, NULL},
+        {"flags", d_flags, sizeof(uint32_t), NULL},
+    };
+    const int n_out = (int)(sizeof out / sizeof out[0]);
+    for (int i = 0; i < n_out; ++i) {
+        out[i].host = to_host(out[i].dev, out[i].bytes);
+        write_file(out[i].name, out[i].host, out[i].bytes);
+    }
+
+    if (graph) {
+        /* the same three calls captured once; the library allocates, synchronises and memsets
+           nothing, so the captured graph holds only its kernels */
+        hipGraph_t g;
+        hipGraphExec_t exec;
+        hip_ok(hipStreamBeginCapture(stream, hipStreamCaptureModeGlobal), "hipStreamBeginCapture");
+        STEP();
+        hip_ok(hipStreamEndCapture(stream, &g), "hipStreamEndCapture");
+        hip_ok(hipGraphInstantiate(&exec, g, NULL, NULL, 0), "hipGraphInstantiate");
+        for (int rep = 0; rep < 3; ++rep) {
+            /* outputs overwritten outside the graph: a sentinel, and the flag word cleared */
+            for (int i = 0; i < n_out; ++i)
+                if (out[i].bytes)
+                    hip_ok(hipMemset(out[i].dev, i == n_out - 1 ? 0 : 0xA5, out[i].bytes), "hipMemset");
+            hip_ok(hipGraphLaunch(exec, stream), "hipGraphLaunch");
+            hip_ok(hipStreamSynchronize(stream), "hipStreamSynchronize");
+            for (int i = 0; i < n_out; ++i)
+                if (!same_as(out[i].dev, out[i].host, out[i].bytes)) die("graph replay differs", out[i].name);
+        }
+        hip_ok(hipGraphExecDestroy(exec), "hipGraphExecDestroy");
+        hip_ok(hipGraphDestroy(g), "hipGraphDestroy");
+        printf("c_client: graph of the step replayed 3 times, every output equal to the eager run\n");
+    }
+#undef STEP
     hip_ok(hipStreamDestroy(stream), "hipStreamDestroy");
     printf("c_client: R=%d T=%d N=%lld V=%d unit=%d ws=%zu bytes: ok\n", R, T, N, V, unit, ws_bytes);
     return 0;

@@ -1,7 +1,8 @@
 """The C ABI from plain C: tests/c_client.c (built by tests/c_client_build.py) reads a reduced
 workload from files, runs stride_score -> stride_stop -> stride_restart_turn through libstride.so
 with device memory from hipMalloc, and writes its outputs; they are compared with the float64
-oracle element by element.  Nothing on the client's side of the boundary is Python or torch."""
+oracle element by element.  Nothing on the client's side of the boundary is Python or torch.
+With --graph the client also captures the step into a HIP graph and checks its replays."""
 import os
 import subprocess
 import sys
@@ -62,6 +63,18 @@ def _read_outputs(wl, d):
     ("reasoning", 2003, dict(R=2, tok=700, vocab=999), [0, 150]),
 ])
 def test_c_client_matches_the_oracle(name, seed, scale, start, tmp_path):
+    _client_against_the_oracle(name, seed, scale, start, tmp_path, graph=False)
+
+
+def test_c_client_graph_replay(tmp_path):
+    """The client captures score -> stop -> restart into a HIP graph with hipStreamBeginCapture,
+    overwrites every output, replays the graph three times and requires each replay to equal its
+    eager run bit for bit; the eager outputs are compared with the oracle as above."""
+    _client_against_the_oracle("agentic", 2004, dict(R=3, turns=4, tok_lo=10, tok_hi=50, vocab=777),
+                               [0, 1, 0], tmp_path, graph=True)
+
+
+def _client_against_the_oracle(name, seed, scale, start, tmp_path, graph):
     assert os.path.exists(CB.BIN), f"{CB.BIN} is missing: build() compiles it"
     wl = W.make(name, seed=seed, scale=scale)
     if start is not None:
@@ -72,9 +85,12 @@ def test_c_client_matches_the_oracle(name, seed, scale, start, tmp_path):
     lam, alpha = H.thresholds(wl, sc)
     ora = {r: (sc[r], H.oracle_rollout(wl, r, sc[r], lam, alpha)) for r in sc}
     _write_inputs(wl, lam, alpha, str(tmp_path))
-    r = subprocess.run([CB.BIN, str(tmp_path)], capture_output=True, text=True, timeout=120)
+    r = subprocess.run([CB.BIN, str(tmp_path)] + (["--graph"] if graph else []),
+                       capture_output=True, text=True, timeout=120)
     say(r.stdout.strip(), r.stderr.strip())
     assert r.returncode == 0, r.stderr
+    if graph:
+        assert "replayed 3 times" in r.stdout, r.stdout
     out = _read_outputs(wl, str(tmp_path))
     assert out["flags"] == 0, hex(out["flags"])
     rep = H.compare(wl, out, ora, lam, alpha)
