@@ -305,8 +305,9 @@ stride_status stride_records_plan(stride_records *rec, int32_t n_tasks, const in
 /* Streaming-read reference (a measurement aid, not a step of the method).
  *
  * Reads n_rows rows of `a` (and, when b is not NULL, the same rows of `b`,
- * interleaved row by row) with the scoring kernel's access pattern -- one
- * wavefront per row, 16-byte non-temporal loads -- and does no arithmetic, so
+ * interleaved row by row) with the scoring kernel's access pattern for batches of
+ * 16,384 row items or more -- one wavefront per row, 16-byte non-temporal loads
+ * -- and does no arithmetic, so
  * timing it gives the read bandwidth that pattern reaches; the scoring kernel's
  * bandwidth is reported as a fraction of it next to the fraction of peak.
  *   a, b        device rows, 16-byte aligned; b may be NULL
