@@ -135,3 +135,50 @@ def test_online_turn_by_turn_scoring_matches_batch_path():
     assert int(flags.item()) == 0
     assert st_stop.cpu().numpy().tolist() == batch.stop_unit.cpu().numpy().tolist()
     say(f"[online turn-by-turn] stops {st_stop.cpu().numpy().tolist()}")
+
+
+def test_online_two_hundred_thousand_rollouts():
+    """200,000 rollout slots over 64 domains, each fed one turn mean per call; each call takes a
+    random 80% of the rollouts that still have turns, in shuffled slot order.  The carried state
+    gives the oracle's batch stop for every rollout, and the carried sum at each stop."""
+    import torch
+    import paper_2609_14636_amd as P
+    g = np.random.default_rng(200000)
+    R, K, D = 200000, 5, 64
+    sizes = np.full(R, K)
+    off = (np.arange(R + 1) * K).astype(np.int64)
+    vals = -np.abs(g.normal(1.0, 0.7, size=R * K))
+    dom = g.integers(0, D, size=R).astype(np.int32)
+    lam = list(-2.0 - 0.05 * np.arange(D))
+    cum_o, stop_o, _ = H.OP.O.stop(off, vals, np.array(lam)[dom], None)
+    st_cum = torch.zeros(R, dtype=torch.float64, device="cuda")
+    st_units = torch.zeros(R, dtype=torch.int32, device="cuda")
+    st_stop = torch.full((R,), -1, dtype=torch.int32, device="cuda")
+    flags = torch.zeros(1, dtype=torch.int32, device="cuda")
+    dom_d = torch.from_numpy(dom).cuda()
+    pos = np.zeros(R, np.int64)
+    calls = 0
+    while (pos < sizes).any():
+        left = np.nonzero(pos < sizes)[0]
+        active = left[g.random(left.size) < 0.8]
+        if active.size == 0:
+            continue
+        g.shuffle(active)
+        v = torch.from_numpy(vals[off[active] + pos[active]]).cuda()
+        P.stride_stop_step(torch.from_numpy(active.astype(np.int32)).cuda(),
+                           torch.arange(active.size + 1, dtype=torch.int64).cuda(), W.UNIT_TURN, v,
+                           dom_d, lam, st_cum, st_units, st_stop, flags)
+        pos[active] += 1
+        calls += 1
+    torch.cuda.synchronize()
+    assert int(flags.item()) == 0
+    s, c = st_stop.cpu().numpy(), st_cum.cpu().numpy()
+    same = s == stop_o
+    for r in np.nonzero(~same)[0]:
+        hi = K if (s[r] < 0 or stop_o[r] < 0) else max(s[r], stop_o[r]) + 1
+        assert np.any(np.abs(cum_o[off[r]:off[r] + hi] - lam[dom[r]]) <= H.BAND), r
+    hit = same & (s >= 0)
+    want = cum_o[off[:-1][hit] + s[hit]]
+    assert np.all(np.abs(c[hit] - want) <= 1e-9 * np.maximum(np.abs(want), 1.0))
+    assert np.array_equal(st_units.cpu().numpy(), sizes)
+    say(f"[online 200k] {calls} calls, stops equal {int(same.sum())}/{R}, stopped {int((s >= 0).sum())}")
