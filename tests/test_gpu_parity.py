@@ -321,6 +321,19 @@ def test_stop_and_restart_many_tiles(seed):
     _stop_restart_vs_oracle(g, sizes, [-40.0, -400.0, -4000.0], [-0.9, -1.5, -np.inf], "scan")
 
 
+def test_stop_and_restart_with_non_finite_and_extreme_thresholds():
+    """lambda = +inf stops at the first unit counted, -inf and NaN never stop (the strict test is
+    false), 0 and +-1e-300 sit at the edge of the sums' sign; alpha = +inf and NaN make no unit
+    correct (K_max = 0, k* = -1), -inf makes every masked-in unit correct.  Exact against the
+    oracle: no value lies within the band of these thresholds."""
+    g = np.random.default_rng(77)
+    sizes = g.integers(1, 60, size=3000)
+    lam = [np.inf, -np.inf, np.nan, 0.0, -1e-300, 1e-300]
+    alpha = [np.inf, -np.inf, np.nan, 0.0, -0.5, -1e300]
+    s = _stop_restart_vs_oracle(g, sizes, lam, alpha, "extreme thresholds")
+    assert (s >= 0).any() and (s < 0).any()
+
+
 def test_stop_and_restart_a_million_short_rollouts():
     """One million rollouts of one to five units: hundreds of rollout starts in every scan tile,
     a restart launch of a million workgroups, and 64 domains of lambda and alpha."""
