@@ -235,6 +235,33 @@ def check_stop_golden():
             assert ret.tolist() == case["retained"], (case["name"], ret.tolist())
 
 
+def check_thresholds_at_the_extremes():
+    """Eq. (5)'s strict test and Sec. 4.2's gate at thresholds that decide every unit alike:
+    lambda = +inf stops at the first unit counted (K0), lambda = -inf or NaN never stops (a
+    comparison with NaN is false); alpha = +inf or NaN makes no unit correct, so K_max = 0, k* = -1
+    and K0 = 0, while alpha = -inf leaves only the mask, so with every unit masked in K_max is the
+    whole record and k* its first minimum."""
+    rng = np.random.default_rng(31)
+    for _ in range(100):
+        n = int(rng.integers(1, 20))
+        vals = -np.abs(rng.normal(1.0, 1.0, size=n))
+        k0 = int(rng.integers(0, n))
+        off, st = np.array([0, n]), np.array([k0], np.int32)
+        _, stop, _ = O.stop(off, vals, np.array([np.inf]), st)
+        assert stop[0] == k0
+        for lam in (-np.inf, np.nan):
+            _, stop, _ = O.stop(off, vals, np.array([lam]), st)
+            assert stop[0] == -1
+        rl = np.array([int(rng.integers(0, n + 1))], np.int32)
+        for alpha in (np.inf, np.nan):
+            ks, k0s, km = O.restart(off, vals, rl, np.array([alpha]), None)
+            assert (ks[0], k0s[0], km[0]) == (-1, 0, 0)
+        ks, k0s, km = O.restart(off, vals, rl, np.array([-np.inf]), np.ones(n, np.uint8))
+        assert km[0] == rl[0]
+        want = int(np.argmin(vals[:rl[0]])) if rl[0] > 0 else -1
+        assert ks[0] == want and k0s[0] == max(want, 0)
+
+
 # ---------------------------------------------------------------- restart pick (Sec. 4.2, Eq. 6)
 
 def check_restart_golden():
@@ -390,4 +417,4 @@ def check_retained_mask():
     assert m.tolist() == [0, 0, 1, 1, 0, 0, 1, 1, 0]
 
 
-ALL_CHECKS += [check_opd_grad_finite_differences, check_retained_mask]
+ALL_CHECKS += [check_opd_grad_finite_differences, check_retained_mask, check_thresholds_at_the_extremes]
