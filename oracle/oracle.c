@@ -107,7 +107,7 @@ int oracle_logp_rows(int64_t n_rows, int64_t vocab, int64_t ld, int dtype,
 /*
  * Per-token signals of Sec. 3.1-3.2 from the two sampled-token
  * log-probabilities: the OPD reward r_t = log pi_T - log pi_theta (Eq. 1) and
- * the per-token student-teacher KL estimate log pi_theta - log pi_T = -r_t
+ * each token's KL estimate between student and teacher, log pi_theta - log pi_T = -r_t
  * (Sec. 3.2, analysis set-up).  kl may alias neither input.
  */
 void oracle_token_kl(int64_t n, const double *logp_s, const double *logp_t, double *kl) {
@@ -145,7 +145,7 @@ void oracle_exact_kl(int64_t n_rows, int64_t vocab, int64_t ld, int dtype,
 }
 
 /*
- * Per-turn mean teacher log-probability, Eq. (4) (Sec. 3.1): for turn k with
+ * Mean teacher log-probability of each turn, Eq. (4) (Sec. 3.1): for turn k with
  * tokens [turn_tok_off[k], turn_tok_off[k+1]), lbar_k = (1/n_k) sum_i
  * logp_t[i].  An empty turn (n_k = 0) has no mean: NaN and OR_EMPTY_TURN.
  * Offsets that decrease also give NaN and OR_EMPTY_TURN.

@@ -122,7 +122,7 @@ def exact_kl(teacher: np.ndarray, student: np.ndarray, vocab: int | None = None)
 
 
 def turn_mean(turn_tok_off: np.ndarray, logp_t: np.ndarray):
-    """Per-turn mean teacher log-probability, Eq. (4).  Returns (means, flags)."""
+    """Mean teacher log-probability of each turn, Eq. (4).  Returns (means, flags)."""
     off = np.ascontiguousarray(turn_tok_off, dtype=np.int64)
     logp_t = np.ascontiguousarray(logp_t, dtype=np.float64)
     t = off.size - 1

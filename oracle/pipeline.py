@@ -3,8 +3,8 @@
 TEST INFRASTRUCTURE ONLY (tests, smoke check, CPU-baseline leg of the benchmark).
 
 The steps follow the paper in order: sampled-token log-probabilities of teacher
-and student and the per-token KL estimate (Eq. 1, Sec. 3.2), per-turn mean
-teacher log-probability (Eq. 4), the early-stop test (Eq. 5, Sec. 4.1; token
+and student and each token's KL estimate (Eq. 1, Sec. 3.2), the mean teacher
+log-probability of each turn (Eq. 4), the early-stop test (Eq. 5, Sec. 4.1; token
 units for the single-turn variant of Sec. 5.5), then the prefix-buffer restart
 pick over the record of generated units (Sec. 4.2, Eq. 6, Algorithm 1).
 """

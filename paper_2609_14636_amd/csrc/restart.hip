@@ -1,9 +1,9 @@
 // restart.hip -- prefix-buffer restart pick of the weakest correct unit.
 //
 // Sec. 4.2 step 1: unit k is correct iff its value exceeds alpha (strictly),
-// here also requiring its correctness-mask bit.  Step 2 and Eq. (6): K_max is
-// the length of the longest continuous correct prefix, k* the argmin of the
-// values over it.  Step 3 and Algorithm 1: the next rollout reuses K0 = k* - 1
+// here also requiring its correctness-mask bit.  Step 2 and Eq. (6): K_max
+// counts the correct units from the start of the record up to the first one
+// that is not, and k* is the argmin of the values among those K_max units.  Step 3 and Algorithm 1: the next rollout reuses K0 = k* - 1
 // turns (1-based) as context; a task without a usable prefix starts from 0.
 // The record is the rollout's units up to and including its stop (Algorithm 1
 // records the generated turns).  Ties go to the lowest index.

@@ -1,7 +1,7 @@
-// turn.hip -- per-turn mean teacher log-probability and the per-token KL estimate.
+// turn.hip -- mean teacher log-probability of each turn, and each token's KL estimate.
 //
 // Eq. (4) (Sec. 3.1): lbar_k = (1/n_k) sum over the rows of turn k of
-// log pi_T(y).  Sec. 3.2: the per-token student-teacher KL estimate is
+// log pi_T(y).  Sec. 3.2: each token's KL estimate between student and teacher is
 // log pi_S(y) - log pi_T(y) (= -r_t of Eq. 1), written for the same rows in the
 // same pass.
 //
