@@ -214,6 +214,17 @@ int main(int argc, char **argv) {
     }
 #undef STEP
     hip_ok(hipStreamDestroy(stream), "hipStreamDestroy");
+    /* the caller owns every buffer the library was handed: release them */
+    for (int i = 0; i < n_out; ++i) {
+        free(out[i].host);
+        hip_ok(hipFree(out[i].dev), "hipFree");
+    }
+    const void *inputs[] = {L.rollout_turn_off, L.turn_tok_off, L.domain, d_teacher, d_student,
+                            d_ids, d_start, d_mask, d_ws};
+    for (size_t i = 0; i < sizeof inputs / sizeof inputs[0]; ++i)
+        if (inputs[i]) hip_ok(hipFree((void *)inputs[i]), "hipFree");
+    free(rto), free(tto), free(teacher), free(student), free(ids), free(lambda), free(alpha);
+    free(start), free(mask), free(domain), free(tpad), free(spad);
     printf("c_client: R=%d T=%d N=%lld V=%d unit=%d ws=%zu bytes: ok\n", R, T, N, V, unit, ws_bytes);
     return 0;
 }
