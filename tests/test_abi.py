@@ -60,16 +60,17 @@ def _fake(n):
     return torch.zeros(n, dtype=torch.float32)
 
 
-@pytest.mark.parametrize("case,status", [
-    ("vocab0", P.stride.StrideError), ("ld_small", P.stride.StrideError),
-    ("bad_unit", P.stride.StrideError), ("ws_small", P.stride.StrideError),
-    ("n_dom0", P.stride.StrideError), ("kl_without_student", P.stride.StrideError),
-    ("student_without_logp_s", P.stride.StrideError), ("kl_without_logp_s", P.stride.StrideError),
-    ("kl_full_without_logp_s", P.stride.StrideError),
-    ("fused_student_without_logp_s", P.stride.StrideError),
-    ("fused_kl_without_logp_s", P.stride.StrideError),
+@pytest.mark.parametrize("case,code", [
+    ("vocab0", 1), ("ld_small", 1), ("bad_unit", 1), ("ws_small", 3), ("n_dom0", 2),
+    ("kl_without_student", 1), ("student_without_logp_s", 1), ("kl_without_logp_s", 1),
+    ("kl_full_without_logp_s", 1), ("fused_student_without_logp_s", 1),
+    ("fused_kl_without_logp_s", 1), ("fused_ws_small", 3), ("ws_unaligned", 3),
+    ("n_teachers_65", 2), ("n_dom_65", 2), ("grad_bad_unit", 1),
 ])
-def test_argument_errors_raise_before_launch(case, status):
+def test_argument_errors_raise_before_launch(case, code):
+    """Each bad argument returns its status (1 invalid argument, 2 unsupported, 3 workspace)
+    before anything is launched: the buffers here are host memory, which no kernel could read."""
+    status = P.stride.StrideError
     lay = _layout()
     x = torch.zeros((10, 16), dtype=torch.float32)
     ids = torch.zeros(10, dtype=torch.int32)
@@ -105,8 +106,23 @@ def test_argument_errors_raise_before_launch(case, status):
             xs = torch.zeros((10, 16), dtype=torch.bfloat16)
             kl = out if case == "fused_kl_without_logp_s" else None
             P.stride_score_fused(lay, 16, h, w, xs, ids, out, None, kl, tm, None, ws, stream=0)
-    assert ei.value.status == (3 if case == "ws_small" else (2 if case == "n_dom0" else 1)), \
-        P.library().stride_last_error().decode()
+        elif case == "fused_ws_small":
+            h = torch.zeros((10, 64), dtype=torch.bfloat16)
+            w = torch.zeros((16, 64), dtype=torch.bfloat16)
+            P.stride_score_fused(lay, 16, h, w, None, ids, out, None, None, tm, None,
+                                 torch.zeros(512, dtype=torch.uint8), stream=0)
+        elif case == "ws_unaligned":
+            P.stride_stop(lay, P.STRIDE_UNIT_TOKEN, out, [-1.0], None, tm, ids, None, None,
+                          ws[1:], stream=0)
+        elif case == "n_teachers_65":
+            P.stride_score(lay, 16, [x] * 65, x, ids, out, out, out, tm, None, ws, stream=0)
+        elif case == "n_dom_65":
+            P.stride_stop(lay, P.STRIDE_UNIT_TOKEN, out, [-1.0] * 65, None, tm, ids, None, None,
+                          ws, stream=0)
+        elif case == "grad_bad_unit":
+            P.stride_opd_grad(lay, 7, 16, x, ids, out, out, None, ids, 1.0, x, out, None, ws,
+                              stream=0)
+    assert ei.value.status == code, P.library().stride_last_error().decode()
     assert P.library().stride_last_error().decode()
 
 
