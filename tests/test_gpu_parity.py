@@ -361,6 +361,16 @@ def test_either_side_of_the_shared_row_threshold(n_rows, with_student):
                 assert np.array_equal(gpu[k].view(np.uint8), again[k].view(np.uint8)), k
 
 
+@pytest.mark.parametrize("tok", [500, 1100])
+def test_fp32_rows_either_side_of_the_shared_row_threshold(tok):
+    """fp32 logits (the tiny workload's generator, V = 1024) with 2 rollouts x 4 turns x tok
+    tokens: 8,000 row items run the shared-row kernel, 17,600 the one-wavefront kernel; every
+    row against the oracle."""
+    wl = W.make("tiny", seed=23, scale=dict(R=2, turns=4, tok=tok))
+    assert wl.dtype == W.F32
+    _parity(wl)
+
+
 def test_determinism():
     import torch
     wl = W.make("reasoning", seed=5, scale=dict(R=3, tok=3000, vocab=4096))
