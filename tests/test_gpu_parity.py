@@ -197,11 +197,15 @@ def test_random_small_layouts():
 
 # ---------------------------------------------------------------- data errors (forced from the host)
 
-def test_data_error_flags():
+@pytest.mark.parametrize("pad", [0, 8200])
+def test_data_error_flags(pad):
+    """Non-finite rows and token ids out of range give NaN and flags; with pad, a third rollout of
+    valid rows lifts the batch past 16,384 row items, so the one-wavefront kernel handles the same
+    bad rows that the shared-row kernel handles without it."""
     import torch
     import paper_2609_14636_amd as P
     vocab = 64
-    lengths = [np.array([4, 3]), np.array([5])]
+    lengths = [np.array([4, 3]), np.array([5])] + ([np.array([pad])] if pad else [])
     wl = _custom(3, vocab, W.F32, lengths, start=False, mask=False)
     inp = H.device_inputs(wl)
     t = inp["teachers"][0]
@@ -231,15 +235,20 @@ def test_data_error_flags():
     assert fl == 0 and abs(lp[0] - out["logp_t"][3]) < H.TOL_LOGP
 
 
-def test_empty_turn_and_bad_domain_flags():
+@pytest.mark.parametrize("pad", [0, 8200])
+def test_empty_turn_and_bad_domain_flags(pad):
+    """An empty turn and a rollout routed to a teacher that does not exist; with pad, a third
+    rollout of valid rows moves the batch onto the one-wavefront kernel."""
     import torch
     import paper_2609_14636_amd as P
-    rto = torch.tensor([0, 2, 3], dtype=torch.int32, device="cuda")
-    tto = torch.tensor([0, 4, 4, 6], dtype=torch.int64, device="cuda")  # turn 1 is empty
-    dom = torch.tensor([0, 5], dtype=torch.int32, device="cuda")       # rollout 1: bad domain
-    lay = P.Layout(rto, tto, 6, dom)
-    x = torch.zeros((6, 8), dtype=torch.float32, device="cuda")
-    ids = torch.zeros(6, dtype=torch.int32, device="cuda")
+    rto = torch.tensor([0, 2, 3] + ([4] if pad else []), dtype=torch.int32, device="cuda")
+    tto = torch.tensor([0, 4, 4, 6] + ([6 + pad] if pad else []), dtype=torch.int64,
+                       device="cuda")                                   # turn 1 is empty
+    dom = torch.tensor([0, 5] + ([0] if pad else []), dtype=torch.int32,
+                       device="cuda")                                   # rollout 1: bad domain
+    lay = P.Layout(rto, tto, 6 + pad, dom)
+    x = torch.zeros((6 + pad, 8), dtype=torch.float32, device="cuda")
+    ids = torch.zeros(6 + pad, dtype=torch.int32, device="cuda")
     path = P.Path(lay, W.UNIT_TURN)
     path.run(8, [x, x], x, ids, [-1.0, -1.0], [-5.0, -5.0])
     torch.cuda.synchronize()
@@ -247,6 +256,8 @@ def test_empty_turn_and_bad_domain_flags():
     assert out["flags"] & P.STRIDE_FLAG_EMPTY_TURN and out["flags"] & P.STRIDE_FLAG_BAD_DOMAIN
     assert np.isnan(out["turn_mean"][1]) and abs(out["turn_mean"][0] + math.log(8)) < 1e-6
     assert np.isnan(out["logp_t"][4:6]).all()  # rows of the badly routed rollout
+    if pad:  # the valid rollout is untouched: uniform rows give log(1/8) everywhere
+        assert np.allclose(out["logp_t"][6:], -math.log(8), atol=1e-6)
     assert out["stop_unit"][1] == -1 and out["k_star"][1] == -1 and out["k0"][1] == 0
 
 
