@@ -145,6 +145,26 @@ def test_small_vocab_ragged_parity(vocab, dtype):
     say(f"[ragged V={vocab} dtype={dtype}] {rep}")
 
 
+@pytest.mark.parametrize("vocab", [1, 7, 9])
+@pytest.mark.parametrize("dtype", [W.BF16, W.F32])
+def test_small_vocab_on_the_one_wavefront_kernel(vocab, dtype):
+    """The small vocabularies above again, in a batch of 8,400 rows (16,800 row items), so the
+    one-wavefront kernel's tail handling (a row shorter than one 16-byte word, or one word and a
+    ragged tail) is compared with the oracle too."""
+    g = np.random.default_rng(vocab * 100 + dtype)
+    lengths = [g.integers(200, 500, size=3) for _ in range(7)]
+    total = sum(int(l.sum()) for l in lengths)
+    lengths.append(np.array([8400 - total]))
+    wl = _custom(vocab * 10 + dtype + 7, vocab, dtype, lengths, n_teachers=2)
+    assert 2 * wl.n_tokens >= 16384
+    sc = H.oracle_scores(wl, range(wl.n_rollouts))
+    lam, alpha = _custom_thresholds(wl, sc)
+    ora = {r: (sc[r], H.oracle_rollout(wl, r, sc[r], lam, alpha)) for r in sc}
+    gpu = H.run_gpu(wl, lam, alpha)
+    rep = H.compare(wl, gpu, ora, lam, alpha)
+    say(f"[one-wavefront V={vocab} dtype={dtype}] N={wl.n_tokens} {rep}")
+
+
 @pytest.mark.parametrize("unit", [W.UNIT_TURN, W.UNIT_TOKEN])
 def test_ragged_many_rollouts_token_and_turn_units(unit):
     g = np.random.default_rng(5 + unit)
