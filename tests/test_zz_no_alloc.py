@@ -98,3 +98,38 @@ def test_noalloc_stop_matches_workspace_stop_two_calls():
     stops2, R2 = _compare(0, rto2, tto2, means, dom2, start2, lam2)
     say(f"[noalloc] call 2: {stops2}/{R2} stops, outputs identical")
     assert stops2 > 0
+
+
+def test_noalloc_stop_at_the_largest_layout_it_takes():
+    """The largest layout of two-token rollouts whose scratch (256 + 8 (R + 1) + 16 ceil(U / 2048)
+    bytes, each part rounded up to 256) fits the fixed 1 MiB array: accepted, and equal to
+    stride_stop bit for bit; one more rollout is rejected before any launch."""
+    import paper_2609_14636_amd as P
+    r256 = lambda x: (x + 255) // 256 * 256  # noqa: E731
+    need = lambda R: 256 + r256(8 * (R + 1)) + r256(16 * ((2 * R + 2047) // 2048))  # noqa: E731
+    R = 1
+    while need(R + 1) <= (1 << 20):
+        R += 1
+    assert need(R) <= (1 << 20) < need(R + 1)
+    g = np.random.default_rng(131)
+    rto = np.arange(R + 1, dtype=np.int32)
+    tto = (np.arange(R + 1) * 2).astype(np.int64)
+    vals = (-np.abs(g.normal(1.0, 0.5, size=2 * R))).astype(np.float32)
+    dom = g.integers(0, 2, size=R).astype(np.int32)
+    start = g.integers(0, 2, size=R).astype(np.int32)
+    say(f"[noalloc] largest layout: R={R}, {2 * R} token units, scratch {need(R)} bytes")
+    stops, _ = _compare(1, rto, tto, vals, dom, start, [-1.0, -1.6])
+    say(f"[noalloc] largest layout: {stops}/{R} stops, outputs identical")
+    assert 0 < stops < R
+
+    import torch
+    dev = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()  # noqa: E731
+    R1 = R + 1
+    lay = P.Layout(dev(np.arange(R1 + 1, dtype=np.int32)), dev((np.arange(R1 + 1) * 2).astype(np.int64)),
+                   2 * R1, None)
+    cum = torch.empty(2 * R1, dtype=torch.float64, device="cuda")
+    stop = torch.empty(R1, dtype=torch.int32, device="cuda")
+    v = torch.zeros(2 * R1, dtype=torch.float32, device="cuda")
+    with pytest.raises(P.stride.StrideError) as ei:
+        P.stride_stop_noalloc(lay, 1, v, [-1.0], None, cum, stop, None, None)
+    assert ei.value.status == 2
