@@ -51,6 +51,9 @@ def _per_rollout(wl, sc):
     (2, 2, 24, 151936, 2048),   # the full hidden size and vocabulary on 96 rows
     (1, 2, 16, 1048581, 64),    # 2^20 + 5 entries: 4,097 vocabulary tiles, 8,193 partials per row
     (1, 2, 5, 1, 128),          # a single vocabulary entry: every log-probability is 0
+    (2, 2, 1049, 3000, 128),    # 4,196 rows = 17 row tiles: 16-tile super-rows, the second holding
+                                # one ragged tile
+    (1, 2, 1152, 700, 64),      # 9 row tiles: 8-tile super-rows, the second holding one
 ])
 def test_fused_parity(R, turns, tok, vocab, d):
     wl = W.make("fused", seed=3 + vocab, scale=dict(R=R, turns=turns, tok=tok, vocab=vocab, d=d))
