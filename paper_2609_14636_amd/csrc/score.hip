@@ -29,6 +29,10 @@ constexpr uint8_t kBadDomain = 0xFF;
 // 32,768 items on, where one wavefront per row already fills the chip.
 constexpr int kSplitWaves = 8;
 constexpr int64_t kSplitBelow = 16384;
+// Tokens below which the paired pass (exact KL) shares each token's two rows the same way:
+// measured, the shared form is as fast or faster up to 65,536 tokens (64 tokens: 25 us against
+// 108 us) and 0.7-1.4% slower at 85,185 and 131,072.
+constexpr int64_t kPairSplitBelow = 65536;
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
@@ -338,6 +342,70 @@ struct PairArgs {
     int32_t n_teachers;
 };
 
+// Merge two (max, sum) states of the teacher row and two of the student row, with the
+// student's A rescaled like its sum.
+__device__ __forceinline__ void pair_merge(float &mt, float &zt, float &ms, float &zs, float &am,
+                                           float mt2, float zt2, float ms2, float zs2, float am2) {
+    merge(mt, zt, mt2, zt2);
+    const float mn = fmaxf(ms, ms2);
+    const float ref = (mn == -INFINITY) ? 0.0f : mn;
+    const float f1 = fast_exp2((ms - ref) * kLog2e), f2 = fast_exp2((ms2 - ref) * kLog2e);
+    zs = zs * f1 + zs2 * f2;
+    am = am * f1 + am2 * f2;
+    ms = mn;
+}
+
+// The 64 lane states of a wavefront merged by a fixed butterfly of cross-lane shuffles.
+__device__ __forceinline__ void pair_wave_merge(float &mt, float &zt, float &ms, float &zs, float &am) {
+#pragma unroll
+    for (int o = kWave / 2; o > 0; o >>= 1) {
+        const float mt2 = __shfl_xor(mt, o, kWave), zt2 = __shfl_xor(zt, o, kWave);
+        const float ms2 = __shfl_xor(ms, o, kWave), zs2 = __shfl_xor(zs, o, kWave);
+        const float am2 = __shfl_xor(am, o, kWave);
+        pair_merge(mt, zt, ms, zs, am, mt2, zt2, ms2, zs2, am2);
+    }
+}
+
+// The token's exact KL and both sampled-token log-probabilities from the merged states.
+template <int DT>
+__device__ __forceinline__ void write_pair(const PairArgs &a, int64_t row, const u32x4 *pt,
+                                           const u32x4 *ps, float mt, float zt, float ms, float zs,
+                                           float am) {
+    const int32_t y = a.ids[row];
+    uint32_t bad = 0;
+    const bool fin_t = (mt > -INFINITY) && (mt < INFINITY) && (zt > 0.0f) && (zt < INFINITY);
+    const bool fin_s = (ms > -INFINITY) && (ms < INFINITY) && (zs > 0.0f) && (zs < INFINITY);
+    if (!fin_t || !fin_s) bad |= STRIDE_FLAG_NONFINITE;
+    const float lt = __builtin_amdgcn_logf(zt) * kLn2, ls = __builtin_amdgcn_logf(zs) * kLn2;
+    // sum_v p_S (log p_S - log p_T) = A/Z_S - (m_S + log Z_S) + (m_T + log Z_T)
+    // +inf when the teacher gives no mass where the student has some
+    float kl = bad ? __builtin_nanf("") : (am / zs - (ms - mt)) - (ls - lt);
+    if (!(kl == kl)) bad |= STRIDE_FLAG_NONFINITE;
+    // KL >= 0 (Gibbs); when the two rows differ by a constant the fp32 terms cancel to a
+    // rounding residue of either sign, and clamping only reduces that error (NaN stays NaN)
+    if (kl < 0.0f) kl = 0.0f;
+    a.kl_full[row] = kl;
+    if (y < 0 || y >= a.vocab) bad |= STRIDE_FLAG_TOKEN_OOB;
+    float rt, rs;
+    if (bad & (STRIDE_FLAG_TOKEN_OOB | (fin_t && fin_s ? 0u : STRIDE_FLAG_NONFINITE))) {
+        rt = rs = __builtin_nanf("");
+    } else {
+        float xt, xs;
+        if (DT == STRIDE_BF16) {
+            xt = __uint_as_float((uint32_t)(reinterpret_cast<const uint16_t *>(pt)[y]) << 16);
+            xs = __uint_as_float((uint32_t)(reinterpret_cast<const uint16_t *>(ps)[y]) << 16);
+        } else {
+            xt = reinterpret_cast<const float *>(pt)[y];
+            xs = reinterpret_cast<const float *>(ps)[y];
+        }
+        rt = fminf((xt - mt) - lt, 0.0f);  // at most 0, as in score_rows_kernel
+        rs = fminf((xs - ms) - ls, 0.0f);
+    }
+    if (bad) raise_flag(a.flags, bad);
+    a.logp_t[row] = rt;
+    a.logp_s[row] = rs;
+}
+
 template <int DT, int U>
 __global__ __launch_bounds__(256) void score_pairs_kernel(PairArgs a) {
     constexpr int E = Elem<DT>::kPerVec;
@@ -396,53 +464,86 @@ __global__ __launch_bounds__(256) void score_pairs_kernel(PairArgs a) {
             }
         fold_pair<E>(mt, zt, ms, zs, am, xt, xs);
     }
-#pragma unroll
-    for (int o = kWave / 2; o > 0; o >>= 1) {
-        const float mt2 = __shfl_xor(mt, o, kWave), zt2 = __shfl_xor(zt, o, kWave);
-        const float ms2 = __shfl_xor(ms, o, kWave), zs2 = __shfl_xor(zs, o, kWave);
-        const float am2 = __shfl_xor(am, o, kWave);
-        merge(mt, zt, mt2, zt2);
-        const float mn = fmaxf(ms, ms2);
-        const float ref = (mn == -INFINITY) ? 0.0f : mn;
-        const float f1 = fast_exp2((ms - ref) * kLog2e), f2 = fast_exp2((ms2 - ref) * kLog2e);
-        zs = zs * f1 + zs2 * f2;
-        am = am * f1 + am2 * f2;
-        ms = mn;
-    }
-    if (lane == 0) {
-        const int32_t y = a.ids[row];
-        uint32_t bad = 0;
-        const bool fin_t = (mt > -INFINITY) && (mt < INFINITY) && (zt > 0.0f) && (zt < INFINITY);
-        const bool fin_s = (ms > -INFINITY) && (ms < INFINITY) && (zs > 0.0f) && (zs < INFINITY);
-        if (!fin_t || !fin_s) bad |= STRIDE_FLAG_NONFINITE;
-        const float lt = __builtin_amdgcn_logf(zt) * kLn2, ls = __builtin_amdgcn_logf(zs) * kLn2;
-        // sum_v p_S (log p_S - log p_T) = A/Z_S - (m_S + log Z_S) + (m_T + log Z_T)
-        // +inf when the teacher gives no mass where the student has some
-        float kl = bad ? __builtin_nanf("") : (am / zs - (ms - mt)) - (ls - lt);
-        if (!(kl == kl)) bad |= STRIDE_FLAG_NONFINITE;
-        // KL >= 0 (Gibbs); when the two rows differ by a constant the fp32 terms cancel to a
-        // rounding residue of either sign, and clamping only reduces that error (NaN stays NaN)
-        if (kl < 0.0f) kl = 0.0f;
-        a.kl_full[row] = kl;
-        if (y < 0 || y >= a.vocab) bad |= STRIDE_FLAG_TOKEN_OOB;
-        float rt, rs;
-        if (bad & (STRIDE_FLAG_TOKEN_OOB | (fin_t && fin_s ? 0u : STRIDE_FLAG_NONFINITE))) {
-            rt = rs = __builtin_nanf("");
-        } else {
-            float xt, xs;
-            if (DT == STRIDE_BF16) {
-                xt = __uint_as_float((uint32_t)(reinterpret_cast<const uint16_t *>(pt)[y]) << 16);
-                xs = __uint_as_float((uint32_t)(reinterpret_cast<const uint16_t *>(ps)[y]) << 16);
-            } else {
-                xt = reinterpret_cast<const float *>(pt)[y];
-                xs = reinterpret_cast<const float *>(ps)[y];
-            }
-            rt = fminf((xt - mt) - lt, 0.0f);  // at most 0, as in score_rows_kernel
-            rs = fminf((xs - ms) - ls, 0.0f);
+    pair_wave_merge(mt, zt, ms, zs, am);
+    if (lane == 0) write_pair<DT>(a, row, pt, ps, mt, zt, ms, zs, am);
+}
+
+// The paired pass for small batches, as score_rows_split_kernel does for single rows: the
+// kSplitWaves wavefronts of a workgroup share one token's teacher and student rows (chunks w,
+// w + kSplitWaves, ...) and merge their five-value states in wavefront order through LDS.
+template <int DT, int U>
+__global__ __launch_bounds__(kSplitWaves *kWave) void score_pairs_split_kernel(PairArgs a) {
+    constexpr int E = Elem<DT>::kPerVec;
+    __shared__ float s_st[5][kSplitWaves];
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wave = threadIdx.x / kWave;
+    const int64_t row = blockIdx.x;  // one workgroup per token: the grid has exactly n_rows
+    const int d = a.row_dom ? (int)a.row_dom[row] : 0;
+    if (d >= a.n_teachers) {  // the same for the whole workgroup: it leaves before any barrier
+        if (threadIdx.x == 0) {
+            a.logp_t[row] = __builtin_nanf("");
+            a.kl_full[row] = __builtin_nanf("");
+            a.logp_s[row] = __builtin_nanf("");
         }
-        if (bad) raise_flag(a.flags, bad);
-        a.logp_t[row] = rt;
-        a.logp_s[row] = rs;
+        return;
+    }
+    const size_t off = (size_t)row * a.ld * Elem<DT>::kSize;
+    const u32x4 *pt = reinterpret_cast<const u32x4 *>(static_cast<const char *>(a.teachers.p[d]) + off);
+    const u32x4 *ps = reinterpret_cast<const u32x4 *>(static_cast<const char *>(a.student) + off);
+    const int64_t nvec = a.vocab / E;
+    const int tail = a.vocab % E;
+    constexpr int64_t kStep = (int64_t)U * kWave;
+    const int64_t nfull = nvec / kStep;
+    float mt = -INFINITY, zt = 0.0f, ms = -INFINITY, zs = 0.0f, am = 0.0f;
+    for (int64_t c = wave; c < nfull; c += kSplitWaves) {
+        const int64_t k = c * kStep;
+        u32x4 vt[U], vs[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            vt[u] = __builtin_nontemporal_load(pt + k + u * kWave + lane);
+            vs[u] = __builtin_nontemporal_load(ps + k + u * kWave + lane);
+        }
+        float xt[U * E], xs[U * E];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            unpack<DT>(vt[u], xt + u * E);
+            unpack<DT>(vs[u], xs + u * E);
+        }
+        fold_pair<U * E>(mt, zt, ms, zs, am, xt, xs);
+    }
+    for (int64_t k = nfull * kStep + (int64_t)wave * kWave; k < nvec; k += (int64_t)kSplitWaves * kWave) {
+        if (k + lane < nvec) {
+            float xt[E], xs[E];
+            unpack<DT>(__builtin_nontemporal_load(pt + k + lane), xt);
+            unpack<DT>(__builtin_nontemporal_load(ps + k + lane), xs);
+            fold_pair<E>(mt, zt, ms, zs, am, xt, xs);
+        }
+    }
+    if (tail && wave == 0 && lane == 0) {
+        float xt[E], xs[E];
+        unpack<DT>(pt[nvec], xt);
+        unpack<DT>(ps[nvec], xs);
+#pragma unroll
+        for (int j = 0; j < E; ++j)
+            if (j >= tail) {
+                xt[j] = -INFINITY;
+                xs[j] = -INFINITY;
+            }
+        fold_pair<E>(mt, zt, ms, zs, am, xt, xs);
+    }
+    pair_wave_merge(mt, zt, ms, zs, am);
+    if (lane == 0) {
+        s_st[0][wave] = mt;
+        s_st[1][wave] = zt;
+        s_st[2][wave] = ms;
+        s_st[3][wave] = zs;
+        s_st[4][wave] = am;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {  // wave 0's state, then waves 1, 2, ... in order
+        for (int w = 1; w < kSplitWaves; ++w)
+            pair_merge(mt, zt, ms, zs, am, s_st[0][w], s_st[1][w], s_st[2][w], s_st[3][w], s_st[4][w]);
+        write_pair<DT>(a, row, pt, ps, mt, zt, ms, zs, am);
     }
 }
 
@@ -514,6 +615,15 @@ hipError_t launch_score_pairs(int32_t dtype, const PtrTable &teachers, int32_t n
     a.ld = ld;
     a.vocab = vocab;
     a.n_teachers = n_teachers;
+    if (n_rows < kPairSplitBelow) {
+        if (dtype == STRIDE_BF16)
+            hipLaunchKernelGGL((score_pairs_split_kernel<STRIDE_BF16, 4>), dim3((unsigned)n_rows),
+                               dim3(kSplitWaves * kWave), 0, stream, a);
+        else
+            hipLaunchKernelGGL((score_pairs_split_kernel<STRIDE_F32, 4>), dim3((unsigned)n_rows),
+                               dim3(kSplitWaves * kWave), 0, stream, a);
+        return hipGetLastError();
+    }
     const int64_t blocks = (n_rows + 3) / 4;
     if (dtype == STRIDE_BF16)
         hipLaunchKernelGGL((score_pairs_kernel<STRIDE_BF16, 4>), dim3((unsigned)blocks), dim3(256), 0,

@@ -54,6 +54,25 @@ def test_exact_kl_parity(name, scale):
     say(f"[kl_full {name}] max |d| = {d:.2e}, mean KL = {want.mean():.3f}")
 
 
+def test_exact_kl_on_the_one_wavefront_kernel():
+    """65,600 tokens (the paired pass shares rows among eight wavefronts only below 65,536), with a
+    ragged vocabulary of 1,001 entries: the exact KL and both log-probabilities of every token
+    against the oracle."""
+    wl = W.make("reasoning", seed=13, scale=dict(R=4, tok=16400, vocab=1001))
+    assert wl.n_tokens >= 65536
+    sc = H.oracle_scores(wl, range(wl.n_rollouts), exact_kl=True)
+    lam, alpha = [-1e9], [-1e9]
+    gpu = H.run_gpu(wl, lam, alpha, exact_kl=True)
+    assert gpu["flags"] == 0, hex(gpu["flags"])
+    want = np.concatenate([sc[r]["kl_full"] for r in range(wl.n_rollouts)])
+    d = np.max(np.abs(gpu["kl_full"] - want))
+    assert d <= TOL_KL_FULL, d
+    for k in ("logp_t", "logp_s"):
+        o = np.concatenate([sc[r][k] for r in range(wl.n_rollouts)])
+        assert np.max(np.abs(gpu[k] - o)) <= H.TOL_LOGP
+    say(f"[kl_full one-wavefront] N={wl.n_tokens} V={wl.vocab}: max |d| = {d:.2e}")
+
+
 def test_exact_kl_zero_for_shifted_teacher_and_inf_entries():
     """Teacher = student + c gives KL = 0; a -inf teacher entry where the student has mass
     gives KL = +inf; a -inf entry in both rows contributes nothing."""
