@@ -336,8 +336,8 @@ stride_status stride_probe_read_flat(const void *a, const void *b, int64_t n_byt
                                      int64_t sink_len, hipStream_t stream);
 
 /* Streaming read+write reference for the OPD gradient's roofline (a measurement aid,
- * not a step of the method): moves n_rows rows as stride_opd_grad does -- one
- * wavefront per row, a 16-byte non-temporal load and store per word -- copying the
+ * not a step of the method): moves n_rows rows as stride_opd_grad does -- eight
+ * wavefronts per row, a 16-byte non-temporal load and store per word -- copying the
  * first copy_bytes of each row of src to dst; a row whose row_mask byte is 0 is
  * written as zeros without being read (row_mask may be NULL: every row copied).
  *   src, dst    device rows of row_bytes (a multiple of 16), 16-byte aligned

@@ -9,8 +9,9 @@
 // probe_flat_kernel reads the same bytes as one contiguous range per matrix in a
 // grid-stride order (the plainest streaming order), to tell the access pattern
 // apart from the footprint.  probe_copy_kernel moves rows as the OPD gradient
-// kernel does: one wavefront per row, a 16-byte non-temporal load and store per
-// word; rows whose mask byte is 0 are written as zeros without being read.
+// kernel does: eight wavefronts per row (wavefront w takes the row's 4-load chunks
+// w, w + 8, ...), a 16-byte non-temporal load and store per word; rows whose mask
+// byte is 0 are written as zeros without being read.
 #include "common.hpp"
 
 namespace stride {
@@ -75,29 +76,37 @@ __global__ __launch_bounds__(256) void probe_flat_kernel(const u32x4 *a, const u
     if ((threadIdx.x & (kWave - 1)) == 0) sink[(int64_t)blockIdx.x * (blockDim.x / kWave) + threadIdx.x / kWave] = x;
 }
 
-__global__ __launch_bounds__(256) void probe_copy_kernel(const char *src, char *dst,
-                                                         const uint8_t *mask, int64_t n_rows,
-                                                         int64_t row_bytes, int64_t nvec) {
+constexpr int kCopyWaves = 8;
+
+__global__ __launch_bounds__(kCopyWaves *kWave) void probe_copy_kernel(const char *src, char *dst,
+                                                                       const uint8_t *mask,
+                                                                       int64_t n_rows,
+                                                                       int64_t row_bytes,
+                                                                       int64_t nvec) {
     const int lane = threadIdx.x & (kWave - 1);
-    const int64_t row = (int64_t)blockIdx.x * (blockDim.x / kWave) + (threadIdx.x / kWave);
+    const int sub = threadIdx.x / kWave;
+    const int64_t row = blockIdx.x;  // the grid has exactly n_rows workgroups
     if (row >= n_rows) return;
     const u32x4 *s = reinterpret_cast<const u32x4 *>(src + row * row_bytes);
     u32x4 *d = reinterpret_cast<u32x4 *>(dst + row * row_bytes);
     if (mask && !mask[row]) {
         const u32x4 z = {0u, 0u, 0u, 0u};
-        for (int64_t k = lane; k < nvec; k += kWave) __builtin_nontemporal_store(z, d + k);
+        for (int64_t k = (int64_t)sub * kWave + lane; k < nvec; k += (int64_t)kCopyWaves * kWave)
+            __builtin_nontemporal_store(z, d + k);
         return;
     }
     constexpr int U = 4;
-    int64_t k = 0;
-    for (; k + U * kWave <= nvec; k += U * kWave) {
+    constexpr int64_t kStep = (int64_t)U * kWave;
+    const int64_t nfull = nvec / kStep;
+    for (int64_t c = sub; c < nfull; c += kCopyWaves) {
+        const int64_t k = c * kStep;
         u32x4 v[U];
 #pragma unroll
         for (int u = 0; u < U; ++u) v[u] = __builtin_nontemporal_load(s + k + u * kWave + lane);
 #pragma unroll
         for (int u = 0; u < U; ++u) __builtin_nontemporal_store(v[u], d + k + u * kWave + lane);
     }
-    for (; k < nvec; k += kWave)
+    for (int64_t k = nfull * kStep + (int64_t)sub * kWave; k < nvec; k += (int64_t)kCopyWaves * kWave)
         if (k + lane < nvec) __builtin_nontemporal_store(__builtin_nontemporal_load(s + k + lane), d + k + lane);
 }
 
@@ -119,7 +128,7 @@ hipError_t launch_probe_flat(const void *a, const void *b, int64_t n_bytes, uint
 hipError_t launch_probe_copy(const void *src, void *dst, const uint8_t *mask, int64_t n_rows,
                              int64_t row_bytes, int64_t copy_bytes, hipStream_t stream) {
     if (n_rows == 0) return hipSuccess;
-    hipLaunchKernelGGL(probe_copy_kernel, dim3((unsigned)((n_rows + 3) / 4)), dim3(256), 0, stream,
+    hipLaunchKernelGGL(probe_copy_kernel, dim3((unsigned)n_rows), dim3(kCopyWaves * kWave), 0, stream,
                        static_cast<const char *>(src), static_cast<char *>(dst), mask, n_rows,
                        row_bytes, copy_bytes / 16);
     return hipGetLastError();
