@@ -353,6 +353,7 @@ def bench_fused(args):
     torch.cuda.synchronize()
     s_stats = stats_ms(ev_s)
     s_bytes = wl.n_tokens * (wl.vocab * 2 + 4 + 4)
+    band_ab = bench_fused_band_ab(args, wl, inp, path, lt, tm, stream) if args.band_ab > 0 else None
     power = power_under_load(step, args.power) if args.power > 0 else None
     flops = 2.0 * wl.n_tokens * wl.fused_d * wl.vocab
     achieved = flops / (k_ms * 1e-3) / 1e12
@@ -385,10 +386,49 @@ def bench_fused(args):
     }
     if power is not None:
         res["power"] = power
+    if band_ab is not None:
+        res["band_order"] = band_ab
     if not args.no_cpu:
         log("[bench] timing the float64 oracle on a bounded sample")
         res["cpu_baseline"] = cpu_baseline_fused(wl, args.cpu_seconds)
     print(json.dumps(res), flush=True)
+
+
+def bench_fused_band_ab(args, wl, inp, path, lt, tm, stream):
+    """The teacher call through libstride_debug.so with one super-row per band (each W slab
+    read from HBM once per 4,096 rows) against the library's own band, launches alternating on
+    one stream; the log-probabilities of the two orders must be equal bit for bit."""
+    import torch
+
+    import paper_2609_14636_amd as P
+
+    dbg = P.stride.debug_library()
+    lt1 = torch.empty_like(lt)
+    ev = {0: [], 1: []}
+    try:
+        for rep in range(args.band_ab + 1):
+            for band in (1, 0):
+                if dbg.stride_debug_fused_band(band) != 0:
+                    raise SystemExit("libstride_debug.so refused the band setting")
+                a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                a.record(stream)
+                P.stride_score_fused(inp["layout"], wl.vocab, inp["hidden"], inp["w"], None,
+                                     inp["ids"], lt1 if band == 1 else lt, None, None, tm,
+                                     path.flags, path.fused_ws, lib=dbg)
+                b.record(stream)
+                if rep > 0:  # the first pair warms up
+                    ev[band].append((a, b))
+        torch.cuda.synchronize()
+    finally:
+        dbg.stride_debug_fused_band(0)
+    if not torch.equal(lt.view(torch.int32), lt1.view(torch.int32)):
+        raise SystemExit("the two tile orders gave different log-probabilities")
+    one, own = stats_ms(ev[1]), stats_ms(ev[0])
+    log(f"[bench] band order: one super-row per band median {one['median']:.3f} ms, "
+        f"the library's band median {own['median']:.3f} ms ({args.band_ab} launches each)")
+    return {"launches_each": args.band_ab, "one_super_row_ms": one, "library_band_ms": own,
+            "speedup_median": one["median"] / own["median"], "outputs_bit_identical": True,
+            "library": "libstride_debug.so (stride_debug_fused_band)"}
 
 
 def bench_online(args):
@@ -613,6 +653,9 @@ def build_parser() -> argparse.ArgumentParser:
     ap.add_argument("--power", type=float, default=0.0, metavar="SECONDS",
                     help="after the timed steps, run the step back to back for SECONDS while "
                          "sampling socket power, clocks and temperature with amd-smi")
+    ap.add_argument("--band-ab", type=int, default=0, metavar="N",
+                    help="with --workload fused: also time the teacher call with one super-row "
+                         "per band against the library's band, N launches each, alternating")
     ap.add_argument("--exact-kl", action="store_true",
                     help="also compute the exact full-vocabulary KL per token (paired kernel)")
     ap.add_argument("--opd-grad", action="store_true",

@@ -370,6 +370,17 @@ stride_status stride_debug_scan_delay(uint64_t seed, uint32_t one_in, uint32_t s
  * Returns STRIDE_ERR_UNSUPPORTED in the product library (libstride.so). */
 stride_status stride_debug_scan_spin_limit(uint32_t limit);
 
+/* Test hook of the fused projection's tile order (not a step of the method).
+ *
+ * In libstride_debug.so (fused projection compiled with STRIDE_FUSED_BAND_HOOK), later
+ * stride_score_fused calls group `band` super-rows of 4,096 rows per band instead of the
+ * library's own choice (as many as fit 128 MiB of h; band = 0 restores it).  The band only
+ * orders the tiles, so every output must be the same bit for bit at any band; the hook lets a
+ * test check that and a benchmark time one order against another.  Process-wide setting.
+ * Returns STRIDE_ERR_INVALID_ARG for band < 0, and STRIDE_ERR_UNSUPPORTED in the product
+ * library (libstride.so). */
+stride_status stride_debug_fused_band(int32_t band);
+
 /* Message for the last non-OK status returned on this thread ("" if none). */
 const char *stride_last_error(void);
 

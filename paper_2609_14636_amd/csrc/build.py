@@ -4,7 +4,8 @@ Each source is compiled by hipcc in parallel, then linked into
 ``paper_2609_14636_amd/libstride.so``.  Packed-FP32 instruction selection is
 switched off for all device code.  A second library for testing,
 ``libstride_debug.so``, links the same objects except that the stop test's scan
-is compiled with its look-back delay hook (STRIDE_SCAN_DELAY_HOOK).
+is compiled with its look-back delay hook (STRIDE_SCAN_DELAY_HOOK) and the fused
+projection with a settable tile-band size (STRIDE_FUSED_BAND_HOOK).
 """
 import os
 import subprocess
@@ -53,13 +54,14 @@ def _link(objs, out: str, verbose: bool) -> None:
 
 def build(verbose: bool = False) -> str:
     os.makedirs(BUILD, exist_ok=True)
-    jobs = [(s, (), "") for s in SOURCES] + [("scan.hip", ("STRIDE_SCAN_DELAY_HOOK",), "_debug")]
+    hooks = {"scan.hip": "STRIDE_SCAN_DELAY_HOOK", "fused.hip": "STRIDE_FUSED_BAND_HOOK"}
+    jobs = [(s, (), "") for s in SOURCES] + [(s, (d,), "_debug") for s, d in hooks.items()]
     with ThreadPoolExecutor(min(8, len(jobs))) as ex:
         objs = list(ex.map(lambda j: _compile(j[0], verbose, j[1], j[2]), jobs))
-    product, debug_scan = objs[:len(SOURCES)], objs[-1]
+    product = objs[:len(SOURCES)]
+    debug = dict(zip(hooks, objs[len(SOURCES):]))
     _link(product, LIB, verbose)
-    _link([debug_scan if SOURCES[i] == "scan.hip" else o for i, o in enumerate(product)],
-          DEBUG_LIB, verbose)
+    _link([debug.get(SOURCES[i], o) for i, o in enumerate(product)], DEBUG_LIB, verbose)
     return LIB
 
 

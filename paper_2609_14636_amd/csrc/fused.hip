@@ -32,11 +32,13 @@
 //   contiguous).
 //   Workgroups are numbered so that the 32 resident on one XCD (dispatch is
 //   round-robin over the 8 XCDs) cover a 4 x 8 block of tiles of a 16 x 16
-//   super-tile, and super-tiles advance along V: each XCD's L2 serves every
-//   H panel slice to 8 tiles and every W slice to 4, and the 16 H panels of a
-//   super-row stay in the last-level cache while W streams past.  With fewer
-//   than 16 (or 8) row tiles the super-tile is 8 x 32 (or 4 x 64) tiles, so
-//   every XCD still has tiles.
+//   super-tile: each XCD's L2 serves every H panel slice to 8 tiles and every
+//   W slice to 4.  Super-rows are grouped in bands (up to 128 MiB of H, eight
+//   super-rows at d = 2,048) and a band is walked one super-column at a time:
+//   the band's H and the current W slab both stay in the 256 MB last-level
+//   cache, so each W slab comes from HBM once per band instead of once per
+//   super-row.  With fewer than 16 (or 8) row tiles the super-tile is 8 x 32
+//   (or 4 x 64) tiles, so every XCD still has tiles.
 // Kernel 2: z_y = h . w_y per row (one wave per row, fp32).
 // Kernel 3: four waves per 64 rows merge each row's V/128 partials (reads
 //   coalesced across rows) and write log pi_T(y) = (z_y - m) - log s.
@@ -60,6 +62,9 @@ constexpr int kBufB = kBM * kRowB;                 // 32 KB: one operand of one 
 constexpr int kBuffers = 5;                        // LDS ring of operand buffers
 constexpr size_t kLdsBytes = (size_t)kBuffers * kBufB;  // 160 KB, the whole LDS
 constexpr int kHalf = 128;                         // vocabulary entries per partial
+// H bytes a band of super-rows may hold in the 256 MB last-level cache beside the W slab
+// it is reading: 128 MiB, eight 4,096-row super-rows at d = 2,048
+constexpr int64_t kBandHBytes = 128ll << 20;
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.69314718055994531f;
 // Third word of a raw buffer descriptor: 32-bit data format, no swizzle; accesses
@@ -74,9 +79,10 @@ struct FusedArgs {
     int32_t vocab;
     int32_t d;
     int32_t n_half;
-    int32_t tiles_m, tiles_n, super_cols;
+    int32_t tiles_m, tiles_n, super_rows, super_cols;
     int32_t xcd_cols;      // XCD blocks per super-tile row: 2, 4 or 8 (the super-tile is
                            // 32 / xcd_cols row tiles by 8 * xcd_cols vocabulary tiles)
+    int32_t band;          // super-rows per band; a band is walked one super-column at a time
 };
 
 __device__ __forceinline__ float ex2(float x) { return __builtin_amdgcn_exp2f(x); }
@@ -122,8 +128,15 @@ __global__ __launch_bounds__(kThreads, 1) void fused_lse_kernel(FusedArgs a) {
     const int xcd = b & 7, s = b >> 3;
     const int S = s >> 5, q = s & 31;
     const int xc = a.xcd_cols, xr = 8 / xc;
-    const int tm = (S / a.super_cols) * (4 * xr) + (xcd / xc) * 4 + (q & 3);
-    const int tn = (S % a.super_cols) * (8 * xc) + (xcd % xc) * 8 + (q >> 2);
+    // super-tile S -> (super-row, super-column): bands of a.band super-rows, each band
+    // walked column by column, so a W slab read from HBM serves the whole band from the
+    // last-level cache while the band's H stays there too
+    const int per_band = a.band * a.super_cols;
+    const int bi = S / per_band, r0 = bi * a.band, idx = S - bi * per_band;
+    const int rows_b = (a.super_rows - r0) < a.band ? (a.super_rows - r0) : a.band;
+    const int sr = r0 + idx % rows_b, sc = idx / rows_b;
+    const int tm = sr * (4 * xr) + (xcd / xc) * 4 + (q & 3);
+    const int tn = sc * (8 * xc) + (xcd % xc) * 8 + (q >> 2);
     if (tm >= a.tiles_m || tn >= a.tiles_n) return;
     const int64_t m0 = (int64_t)tm * kBM;
     const int64_t n0 = (int64_t)tn * kBN;
@@ -387,6 +400,10 @@ __global__ __launch_bounds__(256) void fused_merge_kernel(const float2 *partial,
 
 namespace {
 
+#ifdef STRIDE_FUSED_BAND_HOOK
+std::atomic<int32_t> g_band_override{0};  // super-rows per band; 0: the library's choice
+#endif
+
 // The projection kernel's dynamic LDS (160 KB) is above the default limit; the limit is
 // raised once per device, so later calls (and calls under stream capture) make no
 // attribute call.
@@ -429,6 +446,13 @@ hipError_t launch_fused_teacher(const uint16_t *h, const uint16_t *w, const int3
     const int xr = 8 / a.xcd_cols;
     a.super_cols = (a.tiles_n + 8 * a.xcd_cols - 1) / (8 * a.xcd_cols);
     const int super_rows = (a.tiles_m + 4 * xr - 1) / (4 * xr);
+    a.super_rows = super_rows;
+    const int64_t h_super_row = (int64_t)4 * xr * kBM * d * 2;  // H bytes of one super-row
+    int64_t band = kBandHBytes / h_super_row;
+#ifdef STRIDE_FUSED_BAND_HOOK
+    if (const int32_t o = g_band_override.load()) band = o;
+#endif
+    a.band = (int)(band < 1 ? 1 : (band > super_rows ? super_rows : band));
     a.partial = static_cast<float2 *>(ws);
     float *zy = reinterpret_cast<float *>(static_cast<char *>(ws) +
                                           (size_t)a.n_half * n_rows * sizeof(float2));
@@ -450,3 +474,14 @@ hipError_t launch_fused_teacher(const uint16_t *h, const uint16_t *w, const int3
 }
 
 }  // namespace stride
+
+extern "C" stride_status stride_debug_fused_band(int32_t band) {
+#ifdef STRIDE_FUSED_BAND_HOOK
+    if (band < 0) return STRIDE_ERR_INVALID_ARG;
+    stride::g_band_override.store(band);
+    return STRIDE_OK;
+#else
+    (void)band;
+    return STRIDE_ERR_UNSUPPORTED;
+#endif
+}

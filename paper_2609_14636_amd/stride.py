@@ -119,6 +119,8 @@ def _load(path: str = LIB_PATH):
     lib.stride_debug_scan_delay.restype = i32
     lib.stride_debug_scan_spin_limit.argtypes = [ctypes.c_uint32]
     lib.stride_debug_scan_spin_limit.restype = i32
+    lib.stride_debug_fused_band.argtypes = [ctypes.c_int32]
+    lib.stride_debug_fused_band.restype = i32
     lib.stride_last_error.argtypes = []
     lib.stride_last_error.restype = ctypes.c_char_p
     return lib
@@ -132,8 +134,8 @@ def library() -> ctypes.CDLL:
 
 
 def debug_library() -> ctypes.CDLL:
-    """libstride_debug.so (the stop test's look-back delay hook compiled in), with the same
-    argument types; for tests of the cross-workgroup protocol only."""
+    """libstride_debug.so (the stop test's look-back delay hook and the fused projection's
+    band setting compiled in), with the same argument types; for tests and timing probes only."""
     return _load(DEBUG_LIB_PATH)
 
 
@@ -225,9 +227,9 @@ def stride_score_fused(layout: Layout, vocab: int, hidden_t: torch.Tensor, w_t: 
                        student_logits: torch.Tensor | None, token_ids: torch.Tensor,
                        logp_t: torch.Tensor, logp_s: torch.Tensor | None, kl: torch.Tensor | None,
                        turn_mean: torch.Tensor, dev_flags: torch.Tensor | None,
-                       ws: torch.Tensor | None, stream=None) -> None:
+                       ws: torch.Tensor | None, stream=None, lib: ctypes.CDLL | None = None) -> None:
     ld = student_logits.stride(0) if student_logits is not None else 0
-    _check(_lib.stride_score_fused(layout.c(), int(vocab), hidden_t.shape[1], _ptr(hidden_t),
+    _check((lib or _lib).stride_score_fused(layout.c(), int(vocab), hidden_t.shape[1], _ptr(hidden_t),
                                    _ptr(w_t), _ptr(student_logits), ld, _ptr(token_ids),
                                    _ptr(logp_t), _ptr(logp_s), _ptr(kl), _ptr(turn_mean),
                                    _ptr(dev_flags), _ptr(ws),

@@ -235,3 +235,13 @@ def test_c_client_compiles_against_the_header():
                         "-I", os.path.join(ROOT, "include"), "-I", "/opt/rocm/include",
                         "-D__HIP_PLATFORM_AMD__", src], capture_output=True, text=True)
     assert r.returncode == 0, r.stderr
+
+
+def test_fused_band_hook():
+    """The fused projection's band setting exists only in the test library: the product library
+    returns STRIDE_ERR_UNSUPPORTED, the test library rejects a negative band and takes 0 (the
+    library's own choice); setting it launches nothing."""
+    assert P.library().stride_debug_fused_band(2) == 2
+    dbg = P.stride.debug_library()
+    assert dbg.stride_debug_fused_band(-1) == 1
+    assert dbg.stride_debug_fused_band(0) == 0

@@ -134,3 +134,65 @@ def test_fused_full_size():
     assert np.all(np.abs(gpu["turn_mean"] - expect) < 0.5), (gpu["turn_mean"].min(), expect)
     assert gpu["stop_unit"].tolist() == [5] * wl.n_rollouts, gpu["stop_unit"]
     assert gpu["k_max"].tolist() == [6] * wl.n_rollouts
+
+
+def test_fused_partial_band():
+    """Bands of super-rows walked one super-column at a time, with a partial last band: 8,300 rows
+    are 33 row tiles, three 16-tile super-rows; at d = 8,192 a super-row holds 64 MiB of h, so a
+    band is two super-rows and the third forms a band of its own; V = 4,200 is 17 vocabulary tiles,
+    two super-columns.  The partial table is filled with NaN before the call, so a tile the grid
+    skipped or visited twice shows in the rows it covers.  The first and last row of every row
+    tile, each over the whole vocabulary, against the oracle."""
+    import torch
+    import paper_2609_14636_amd as P
+    wl = W.make("fused", seed=77, scale=dict(R=1, turns=2, tok=4150, vocab=4200, d=8192))
+    assert wl.n_tokens == 8300
+    inp = H.device_inputs_fused(wl)
+    path = P.Path(inp["layout"], wl.unit, with_student=True, fused_vocab=wl.vocab)
+    path.fused_ws.fill_(0xFF)
+    path.score_fused(wl.vocab, inp["hidden"], inp["w"], inp["student"], inp["ids"])
+    torch.cuda.synchronize()
+    gpu = path.host()
+    assert gpu["flags"] == 0, hex(gpu["flags"])
+    rows = np.unique(np.minimum(np.concatenate([np.arange(0, wl.n_tokens, 256),
+                                                np.arange(255, wl.n_tokens + 255, 256)]),
+                                wl.n_tokens - 1))
+    sc, _ = H.oracle_fused_scores(wl, rows)
+    assert sc["flags"] == 0
+    for k in ("logp_t", "logp_s"):
+        dmax = np.max(np.abs(gpu[k][rows] - sc[k]))
+        assert dmax <= H.TOL_LOGP, (k, dmax)
+    say(f"[fused band] {rows.size} rows: max |dlogp_t| = "
+        f"{np.max(np.abs(gpu['logp_t'][rows] - sc['logp_t'])):.2e}")
+
+
+def test_fused_band_order_changes_no_bit():
+    """The band of super-rows only orders the tiles: through libstride_debug.so, bands of 1, 2
+    (the library's choice at d = 8,192) and 3 super-rows give the same log-probabilities, KL and
+    turn means bit for bit, on the partial-band layout (three super-rows, two super-columns)."""
+    import torch
+    import paper_2609_14636_amd as P
+    assert P.library().stride_debug_fused_band(1) == 2  # the product library has no hook
+    dbg = P.stride.debug_library()
+    wl = W.make("fused", seed=78, scale=dict(R=1, turns=2, tok=4150, vocab=4200, d=8192))
+    inp = H.device_inputs_fused(wl)
+    path = P.Path(inp["layout"], wl.unit, with_student=True, fused_vocab=wl.vocab)
+    out = {}
+    try:
+        for band in (0, 1, 3):
+            assert dbg.stride_debug_fused_band(band) == 0
+            path.fused_ws.fill_(0xFF)
+            P.stride.stride_score_fused(inp["layout"], wl.vocab, inp["hidden"], inp["w"],
+                                        inp["student"], inp["ids"], path.logp_t, path.logp_s,
+                                        path.kl, path.turn_mean, path.flags, path.fused_ws,
+                                        lib=dbg)
+            torch.cuda.synchronize()
+            out[band] = {k: getattr(path, k).clone() for k in ("logp_t", "logp_s", "kl", "turn_mean")}
+            assert int(path.flags.item()) == 0
+    finally:
+        dbg.stride_debug_fused_band(0)
+    bits = {torch.float32: torch.int32, torch.float64: torch.int64}
+    for band in (1, 3):
+        for k, v in out[band].items():
+            assert torch.equal(v.view(bits[v.dtype]), out[0][k].view(bits[v.dtype])), (band, k)
+    say("[fused band] bands 1, 2 and 3: every output equal bit for bit")
