@@ -227,7 +227,8 @@ def compare(wl: W.Workload, gpu: dict, ora: dict, lam, alpha, rep: Report | None
 
 
 def assert_invariants(gpu: dict, wl: W.Workload):
-    """Properties that hold at any size: logp <= 0, K0 = max(k*, 0), k* < K_max <= record."""
+    """Properties that hold at any size: logp <= 0 (an output contract: the kernels clamp a
+    rounding excess above 0), K0 = max(k*, 0), k* < K_max <= record."""
     lt = gpu["logp_t"]
     assert np.all(lt[np.isfinite(lt)] <= 0.0)
     if gpu.get("logp_s") is not None:
