@@ -2,9 +2,9 @@
 //
 // Algorithm 1 keeps, for every task x, the per-unit teacher signal of its last
 // rollout ({lbar_k}, the record written after each rollout) and, at the next
-// visit, reads it back to choose where to restart: K_max (longest continuous
-// correct prefix), k* (its weakest unit, Eq. 6) and K0 = k* - 1 turns of reused
-// context (Sec. 4.2 steps 1-3); a task without a record starts from K0 = 0.
+// visit, reads it back to choose where to restart: K_max (the length of the
+// leading run of correct units), k* (the weakest unit of that run, Eq. 6) and
+// K0 (Sec. 4.2 steps 1-3); a task without a record starts from K0 = 0.
 // The store is host memory owned through an opaque handle; all calls are
 // thread-safe (one mutex).  Values are doubles (turn means from stride_score, or
 // token log-probabilities in the single-turn setting), with an optional per-unit
@@ -16,7 +16,7 @@
 #include <unordered_map>
 #include <vector>
 
-#include "common.hpp"
+#include "../../include/stride.h"
 
 struct stride_records {
     std::mutex mu;
