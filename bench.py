@@ -686,6 +686,11 @@ def main():
               "(the path shards by whole rollouts with no exchange between GPUs)", file=sys.stderr)
         sys.exit(2)
 
+    if args.band_ab and args.workload != "fused":
+        print("--band-ab times the fused projection's tile order: use it with --workload fused",
+              file=sys.stderr)
+        sys.exit(2)
+
     import torch
 
     if args.copy_calibration:

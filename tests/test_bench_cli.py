@@ -1,5 +1,6 @@
-"""bench.py's command line on the CPU: more than one GPU is refused with exit status 2 before
-anything touches a device, and the record-store timing runs on the host alone."""
+"""bench.py's command line on the CPU: more than one GPU, and options that do not fit the workload,
+are refused with exit status 2 before anything touches a device, and the record-store timing
+runs on the host alone."""
 import json
 import os
 import subprocess
@@ -34,3 +35,12 @@ def test_default_workload_is_the_largest_logits_streaming_one():
     args = bench.build_parser().parse_args([])
     assert args.workload == "reasoning" and args.gpus == 1
     assert 1 <= args.steps <= 100 and args.warmup >= 1
+
+
+def test_band_order_timing_needs_the_fused_workload():
+    """--band-ab times the fused projection's tile order; with another workload it is refused
+    before anything touches a device."""
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--band-ab", "4"],
+                       capture_output=True, text=True, cwd=ROOT, timeout=120)
+    assert r.returncode == 2
+    assert "--workload fused" in r.stderr
