@@ -107,10 +107,16 @@ def test_argument_errors_raise_before_launch(case, code):
             kl = out if case == "fused_kl_without_logp_s" else None
             P.stride_score_fused(lay, 16, h, w, xs, ids, out, None, kl, tm, None, ws, stream=0)
         elif case == "fused_ws_small":
+            # 256-byte aligned, so the size check (not the alignment check) is what fails
             h = torch.zeros((10, 64), dtype=torch.bfloat16)
             w = torch.zeros((16, 64), dtype=torch.bfloat16)
-            P.stride_score_fused(lay, 16, h, w, None, ids, out, None, None, tm, None,
-                                 torch.zeros(512, dtype=torch.uint8), stream=0)
+            need = P.stride_fused_workspace_size(lay, 16)
+            buf = torch.zeros(need + 256, dtype=torch.uint8)
+            off = (-buf.data_ptr()) % 256
+            small = buf[off:off + need - 8]
+            assert small.data_ptr() % 256 == 0
+            P.stride_score_fused(lay, 16, h, w, None, ids, out, None, None, tm, None, small,
+                                 stream=0)
         elif case == "ws_unaligned":
             P.stride_stop(lay, P.STRIDE_UNIT_TOKEN, out, [-1.0], None, tm, ids, None, None,
                           ws[1:], stream=0)
@@ -123,6 +129,8 @@ def test_argument_errors_raise_before_launch(case, code):
             P.stride_opd_grad(lay, 7, 16, x, ids, out, out, None, ids, 1.0, x, out, None, ws,
                               stream=0)
     assert ei.value.status == code, P.library().stride_last_error().decode()
+    if case == "fused_ws_small":
+        assert "need" in P.library().stride_last_error().decode()
     assert P.library().stride_last_error().decode()
 
 
